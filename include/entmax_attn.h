@@ -1,0 +1,134 @@
+/*
+ * entmax_attn.h -- C ABI of the MI355X (gfx950) alpha-entmax flash attention
+ * library (AdaSplash, arXiv 2502.12082).
+ *
+ * Operation (per batch b, head h; Q, K, V, O in R^{n x d}):
+ *   x_ij  = (alpha-1) * scale * <q_i, k_j>          (Eq. 1 scores in Eq. 2 coordinates)
+ *   tau_i : sum_j [x_ij - tau_i]_+^{1/(alpha-1)} = 1  (Eq. 3; Algorithm 1, Halley-bisection)
+ *   P_ij  = [x_ij - tau_i]_+^{1/(alpha-1)}           (Eq. 2)
+ *   O     = P V                                      (Eq. 1 with pi = alpha-entmax)
+ * and its gradients dQ, dK, dV (Sec. 3.2.2, Eq. 11-13, App. A.2).  Key blocks
+ * whose probabilities are all zero are skipped (block mask, Eq. 8; lookup
+ * tables, Sec. 3.2.1).  Causal attention is top-left aligned (key j <= query i).
+ *
+ * Memory: every tensor argument is a DEVICE pointer (HIP), contiguous,
+ * [batch, heads, seqlen, head_dim] with head_dim fastest unless stated.  The
+ * caller allocates and owns everything; the library never allocates, frees or
+ * synchronises.  Calls are asynchronous on `stream` (a hipStream_t; NULL =
+ * the default stream).  Buffers written by entmax_attn_fwd and read by
+ * entmax_attn_bwd (the residuals) must stay alive and unmodified in between.
+ *
+ * Errors: arguments are checked before anything is launched; on failure
+ * nothing is written and a non-zero ea_status is returned.  NaN/Inf inside
+ * the tensors is not checked and propagates.  No C++ exception crosses this
+ * interface.  All functions are reentrant.
+ */
+#ifndef ENTMAX_ATTN_H
+#define ENTMAX_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EA_OK = 0,
+  EA_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad size or parameter */
+  EA_ERR_UNSUPPORTED = 2, /* head_dim not 64/128, unknown dtype, seqlen too large */
+  EA_ERR_WORKSPACE = 3,   /* workspace smaller than entmax_attn_sizes() says */
+  EA_ERR_HIP = 4          /* a kernel launch failed */
+} ea_status;
+
+typedef enum { EA_BF16 = 0, EA_F32 = 1 } ea_dtype;
+
+/* Problem shape.  seqlen n is the number of queries and of keys (1..131072). */
+typedef struct {
+  int32_t batch, heads, seqlen, head_dim; /* head_dim in {64, 128} */
+  int32_t dtype;                          /* ea_dtype of Q, K, V, dO and O */
+} ea_shape;
+
+typedef struct {
+  float alpha;      /* > 1; 2 = sparsemax, 1.5 = 1.5-entmax; finite */
+  float scale;      /* > 0, finite; usually 1/sqrt(head_dim) */
+  int32_t causal;   /* 0 or 1 */
+  int32_t max_iter; /* Halley-bisection updates after the initial midpoint (Algorithm 1's T), 0..64 */
+  float tol;        /* >= 0: a 128-row workgroup stops once every row has |f(tau)| <= tol */
+  int32_t need_bwd; /* 1: also write o2 for a later entmax_attn_bwd */
+} ea_params;
+
+/*
+ * Forward outputs other than O, consumed by the backward.  T = ceil(n / 64)
+ * blocks of 64 rows; BH = batch * heads.
+ *   tau        fp32  [BH, n]       threshold in Eq. 2 coordinates (x - tau)
+ *   o2         fp32  [BH, n, d]    O^(2) = U V / rowsum(U), U = P^{2-alpha} (App. A.2);
+ *                                  required iff need_bwd
+ *   block_mask u8    [BH, T, T]    1 iff some p in the 64x64 block is > 0 (Eq. 8 at the
+ *                                  returned tau); 0 for causally dead blocks
+ *   q_count    i32   [BH, T]       |Q_i|, key blocks listed for query block i
+ *   q_index    i32   [BH, T, T]    row (b,h,i): Q_i ascending in its first q_count entries
+ *   k_count    i32   [BH, T]       |K_j|, query blocks listed for key block j
+ *   k_index    i32   [BH, T, T]    row (b,h,j): K_j ascending in its first k_count entries
+ *   stats      i32   [BH, ceil(n/128)] optional (may be NULL): K passes run by each
+ *                                  128-row solver workgroup (1 max pass + evaluations)
+ */
+typedef struct {
+  float* tau;
+  float* o2;
+  uint8_t* block_mask;
+  int32_t* q_count;
+  int32_t* q_index;
+  int32_t* k_count;
+  int32_t* k_index;
+  int32_t* stats;
+} ea_residuals;
+
+/* Byte sizes of every residual buffer and of the workspaces. */
+typedef struct {
+  size_t tau, o2, block_mask, q_count, q_index, k_count, k_index, stats;
+  size_t ws_fwd; /* workspace entmax_attn_fwd needs (currently 0) */
+  size_t ws_bwd; /* workspace entmax_attn_bwd needs: fp32 [BH, n] for delta */
+} ea_sizes;
+
+/* Library defaults: alpha 1.5, scale 1/sqrt(64), non-causal, max_iter 12,
+ * tol 1e-5, need_bwd 1. */
+void entmax_attn_default_params(ea_params* p);
+
+/* Fills *out for this shape/params.  Errors as for entmax_attn_fwd's shape
+ * and parameter checks. */
+ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_sizes* out);
+
+/*
+ * Forward: solves tau (Algorithm 1/3), writes the block mask and the lookup
+ * tables, then O (and o2 if need_bwd), visiting only listed key blocks.
+ *   q, k, v  [BH, n, d] in shape->dtype, 16-byte aligned
+ *   o        [BH, n, d] in shape->dtype, 16-byte aligned (written)
+ *   res      residual buffers (written), 4-byte aligned, o2 16-byte aligned
+ *   workspace may be NULL when sizes.ws_fwd == 0
+ * Launches 3 kernels on `stream`.
+ */
+ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const void* q,
+                          const void* k, const void* v, void* o, const ea_residuals* res,
+                          void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Backward: dQ, dK, dV (fp32, [BH, n, d], 16-byte aligned, fully written) of
+ * sum(dO * O), from Q, K, V, dO (shape->dtype) and the residuals of the
+ * matching forward (tau, o2, tables; params must equal the forward's).
+ * workspace: at least sizes.ws_bwd bytes, 16-byte aligned.  Launches 3
+ * kernels on `stream`.
+ */
+ea_status entmax_attn_bwd(const ea_shape* shape, const ea_params* params, const void* q,
+                          const void* k, const void* v, const void* dout,
+                          const ea_residuals* res, float* dq, float* dk, float* dv,
+                          void* workspace, size_t ws_bytes, void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* entmax_attn_status_string(ea_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ENTMAX_ATTN_H */

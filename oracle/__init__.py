@@ -52,7 +52,7 @@ def _load():
         lib.eo_halley_bisection_trace.argtypes = [D, i, d, i, D]
         lib.eo_tau.argtypes = [i, i, D, D, d, d, i, I, i, D, i]
         lib.eo_forward_rows.argtypes = [i, i, D, D, D, d, d, i, D, I, i, D, D, i]
-        lib.eo_block_margin.argtypes = [i, i, D, D, d, d, i, D, D, i]
+        lib.eo_block_margin.argtypes = [i, i, D, D, d, d, i, D, I, i, D, i]
         lib.eo_delta_rows.argtypes = [i, i, D, D, I, i, D]
         lib.eo_dq_rows.argtypes = [i, i, D, D, D, D, d, d, i, D, D, I, i, D, i]
         lib.eo_dkdv_cols.argtypes = [i, i, D, D, D, D, d, d, i, D, D, I, i, D, D, i]
@@ -141,13 +141,16 @@ def head_forward_rows(q, k, v, alpha, scale, causal, tau, rows=None, want_o2=Tru
     return o, o2
 
 
-def head_block_margin(q, k, alpha, scale, causal, tau, nthreads=None):
+def head_block_margin(q, k, alpha, scale, causal, tau, block_rows=None, nthreads=None):
+    """[T, T] block margins max (x_ij - tau_i) over valid pairs; rows of blocks
+    not in block_rows (when given) are NaN."""
     q, k, tau = _f64(q), _f64(k), _f64(tau)
     n, d = q.shape
     T = (n + BLOCK - 1) // BLOCK
-    m = np.empty((T, T))
-    _load().eo_block_margin(n, d, _dp(q), _dp(k), alpha, scale, int(causal), _dp(tau), _dp(m),
-                            nthreads or threads())
+    b, cnt = _idx(block_rows, T)
+    m = np.full((T, T), np.nan)
+    _load().eo_block_margin(n, d, _dp(q), _dp(k), alpha, scale, int(causal), _dp(tau), _ip(b),
+                            cnt, _dp(m), nthreads or threads())
     return m
 
 

@@ -353,14 +353,17 @@ void eo_forward_rows(int n, int d, const double* q, const double* k, const doubl
     run_parallel(&J, fwd_worker, nthreads);
 }
 
+/* margin[I*T + J] for the listed 64-row query blocks I (NULL: all T), every
+ * key block J; reads tau of the rows of those blocks only. */
 void eo_block_margin(int n, int d, const double* q, const double* k, double alpha,
-                     double scale, int causal, const double* tau, double* margin,
-                     int nthreads) {
+                     double scale, int causal, const double* tau, const int32_t* brows,
+                     int nbrows, double* margin, int nthreads) {
     eo_job J;
     memset(&J, 0, sizeof J);
     J.n = n; J.d = d; J.causal = causal; J.alpha = alpha; J.scale = scale;
     J.q = q; J.k = k; J.tau = tau; J.margin = margin;
-    J.count = (n + EO_BLOCK - 1) / EO_BLOCK;
+    J.idx = brows;
+    J.count = brows ? nbrows : (n + EO_BLOCK - 1) / EO_BLOCK;
     run_parallel(&J, margin_worker, nthreads);
 }
 

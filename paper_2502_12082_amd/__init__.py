@@ -1,0 +1,213 @@
+"""alpha-entmax flash attention for MI355X (gfx950): Python binding.
+
+Argument marshalling over the C ABI declared in include/entmax_attn.h; every
+step of the computation runs in the HIP kernels of libentmax_attn.so.  torch
+is used only to own device memory and to name the stream.  There is no CPU
+fallback: importing this module without the built library raises.
+
+    import paper_2502_12082_amd as ea
+    o, res = ea.forward(q, k, v, alpha=1.5, scale=d ** -0.5, causal=False)
+    dq, dk, dv = ea.backward(q, k, v, do, res)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libentmax_attn.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libentmax_attn.so is not built; run `python -m paper_2502_12082_amd.build` "
+                      "(or __graft_entry__.build()) first")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+EA_OK, EA_ERR_INVALID_ARG, EA_ERR_UNSUPPORTED, EA_ERR_WORKSPACE, EA_ERR_HIP = range(5)
+EA_BF16, EA_F32 = 0, 1
+SYMBOLS = ("entmax_attn_default_params", "entmax_attn_sizes", "entmax_attn_fwd",
+           "entmax_attn_bwd", "entmax_attn_status_string")
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32),
+                ("seqlen", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("dtype", ctypes.c_int32)]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_float), ("scale", ctypes.c_float),
+                ("causal", ctypes.c_int32), ("max_iter", ctypes.c_int32),
+                ("tol", ctypes.c_float), ("need_bwd", ctypes.c_int32)]
+
+
+class ResidualPtrs(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_void_p) for f in
+                ("tau", "o2", "block_mask", "q_count", "q_index", "k_count", "k_index", "stats")]
+
+
+class Sizes(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_size_t) for f in
+                ("tau", "o2", "block_mask", "q_count", "q_index", "k_count", "k_index", "stats",
+                 "ws_fwd", "ws_bwd")]
+
+
+_P = ctypes.POINTER
+_v = ctypes.c_void_p
+_lib.entmax_attn_default_params.argtypes = [_P(Params)]
+_lib.entmax_attn_default_params.restype = None
+_lib.entmax_attn_sizes.argtypes = [_P(Shape), _P(Params), _P(Sizes)]
+_lib.entmax_attn_sizes.restype = ctypes.c_int
+_lib.entmax_attn_fwd.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _P(ResidualPtrs), _v,
+                                 ctypes.c_size_t, _v]
+_lib.entmax_attn_fwd.restype = ctypes.c_int
+_lib.entmax_attn_bwd.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _P(ResidualPtrs), _v, _v,
+                                 _v, _v, ctypes.c_size_t, _v]
+_lib.entmax_attn_bwd.restype = ctypes.c_int
+_lib.entmax_attn_status_string.argtypes = [ctypes.c_int]
+_lib.entmax_attn_status_string.restype = ctypes.c_char_p
+
+
+class EntmaxAttnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (
+            where, _lib.entmax_attn_status_string(status).decode(), status))
+
+
+def _check(status: int, where: str):
+    if status != EA_OK:
+        raise EntmaxAttnError(status, where)
+
+
+# --------------------------------------------------------- raw C ABI calls
+
+def default_params() -> Params:
+    p = Params()
+    _lib.entmax_attn_default_params(ctypes.byref(p))
+    return p
+
+
+def entmax_attn_sizes(shape: Shape, params: Params) -> Sizes:
+    z = Sizes()
+    _check(_lib.entmax_attn_sizes(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(z)),
+           "entmax_attn_sizes")
+    return z
+
+
+def entmax_attn_fwd(shape, params, q, k, v, o, res: ResidualPtrs, workspace, ws_bytes, stream):
+    """Raw call; pointers are ints (device addresses), stream an int handle."""
+    return _lib.entmax_attn_fwd(ctypes.byref(shape), ctypes.byref(params), q, k, v, o,
+                                ctypes.byref(res), workspace, ws_bytes, stream)
+
+
+def entmax_attn_bwd(shape, params, q, k, v, dout, res: ResidualPtrs, dq, dk, dv, workspace,
+                    ws_bytes, stream):
+    return _lib.entmax_attn_bwd(ctypes.byref(shape), ctypes.byref(params), q, k, v, dout,
+                                ctypes.byref(res), dq, dk, dv, workspace, ws_bytes, stream)
+
+
+# ------------------------------------------------------ torch conveniences
+
+def _torch():
+    import torch
+    return torch
+
+
+def make_shape(q) -> Shape:
+    torch = _torch()
+    if q.dim() != 4:
+        raise ValueError("expected [batch, heads, seqlen, head_dim]")
+    if q.dtype == torch.bfloat16:
+        dt = EA_BF16
+    elif q.dtype == torch.float32:
+        dt = EA_F32
+    else:
+        raise ValueError("dtype must be bfloat16 or float32")
+    B, H, n, d = q.shape
+    return Shape(B, H, n, d, dt)
+
+
+def make_params(alpha=1.5, scale=None, causal=False, need_bwd=True, max_iter=None, tol=None,
+                head_dim=64) -> Params:
+    p = default_params()
+    p.alpha = float(alpha)
+    p.scale = float(scale if scale is not None else head_dim ** -0.5)
+    p.causal = int(bool(causal))
+    p.need_bwd = int(bool(need_bwd))
+    if max_iter is not None:
+        p.max_iter = int(max_iter)
+    if tol is not None:
+        p.tol = float(tol)
+    return p
+
+
+class Residuals:
+    """Device buffers (torch tensors) that the forward fills and the backward
+    reads, sized by entmax_attn_sizes."""
+
+    def __init__(self, shape: Shape, params: Params, device, with_stats: bool = True):
+        torch = _torch()
+        z = entmax_attn_sizes(shape, params)
+        BH, n, d = shape.batch * shape.heads, shape.seqlen, shape.head_dim
+        T = (n + 63) // 64
+        self.shape, self.params, self.sizes = shape, params, z
+        self.tau = torch.empty(z.tau // 4, dtype=torch.float32, device=device).view(BH, n)
+        self.o2 = (torch.empty(z.o2 // 4, dtype=torch.float32, device=device).view(BH, n, d)
+                   if params.need_bwd else None)
+        self.block_mask = torch.empty(z.block_mask, dtype=torch.uint8, device=device).view(BH, T, T)
+        self.q_count = torch.empty(BH * T, dtype=torch.int32, device=device).view(BH, T)
+        self.q_index = torch.empty(BH * T * T, dtype=torch.int32, device=device).view(BH, T, T)
+        self.k_count = torch.empty(BH * T, dtype=torch.int32, device=device).view(BH, T)
+        self.k_index = torch.empty(BH * T * T, dtype=torch.int32, device=device).view(BH, T, T)
+        self.stats = (torch.empty(z.stats // 4, dtype=torch.int32, device=device)
+                      if with_stats else None)
+
+    def ptrs(self) -> ResidualPtrs:
+        f = lambda t: None if t is None else t.data_ptr()
+        return ResidualPtrs(f(self.tau), f(self.o2), f(self.block_mask), f(self.q_count),
+                            f(self.q_index), f(self.k_count), f(self.k_index), f(self.stats))
+
+
+def _stream_handle(device):
+    return _torch().cuda.current_stream(device).cuda_stream
+
+
+def forward(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_iter=None,
+            tol=None, out=None, res: Residuals | None = None):
+    """O and the residuals for Q, K, V ([B, H, n, d] bf16/fp32 CUDA tensors)."""
+    torch = _torch()
+    for t in (q, k, v):
+        if not t.is_cuda or not t.is_contiguous() or t.shape != q.shape or t.dtype != q.dtype:
+            raise ValueError("q, k, v must be contiguous device tensors of one shape and dtype")
+    shape = make_shape(q)
+    params = make_params(alpha, scale, causal, need_bwd, max_iter, tol, head_dim=q.shape[-1])
+    if res is None:
+        res = Residuals(shape, params, q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    rp = res.ptrs()
+    _check(entmax_attn_fwd(shape, params, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                           out.data_ptr(), rp, None, 0, _stream_handle(q.device)),
+           "entmax_attn_fwd")
+    res.params = params
+    return out, res
+
+
+def backward(q, k, v, dout, res: Residuals, dq=None, dk=None, dv=None, workspace=None):
+    """(dQ, dK, dV) in fp32 for the loss sum(dO * O) of the forward that filled res."""
+    torch = _torch()
+    shape = make_shape(q)
+    if dout.shape != q.shape or dout.dtype != q.dtype or not dout.is_contiguous():
+        raise ValueError("dout must match q")
+    mk = lambda t: t if t is not None else torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    dq, dk, dv = mk(dq), mk(dk), mk(dv)
+    if workspace is None:
+        workspace = torch.empty(max(res.sizes.ws_bwd, 16) // 4 + 4, dtype=torch.float32,
+                                device=q.device)
+    rp = res.ptrs()
+    _check(entmax_attn_bwd(shape, res.params, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                           dout.data_ptr(), rp, dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                           workspace.data_ptr(), workspace.numel() * 4, _stream_handle(q.device)),
+           "entmax_attn_bwd")
+    return dq, dk, dv

@@ -1,0 +1,183 @@
+// ea_api.hip -- the C ABI: argument checks, buffer sizes and the launch
+// sequence of the forward (tau solver -> table compaction -> sparse forward)
+// and backward (delta -> dK/dV -> dQ) passes.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/entmax_attn.h"
+#include "ea_internal.h"
+
+namespace ea {
+
+int gamma_kind(float alpha) {
+  if (alpha == 2.0f) return 1;
+  if (alpha == 1.5f) return 2;
+  if (alpha == 1.25f) return 4;
+  return 0;
+}
+
+namespace {
+
+constexpr int DEFAULT_MAX_ITER = 12;
+constexpr float DEFAULT_TOL = 1e-5f;
+constexpr int MAX_ITER_CAP = 64;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+struct Dims {
+  int64_t BH, n, d, T, elems;
+  int dtype;
+  size_t esize;
+};
+
+ea_status check_shape(const ea_shape* s, const ea_params* p, Dims* out) {
+  if (!s || !p) return EA_ERR_INVALID_ARG;
+  if (s->batch < 1 || s->heads < 1 || s->seqlen < 1 || s->head_dim < 1) return EA_ERR_INVALID_ARG;
+  if (s->dtype != EA_BF16 && s->dtype != EA_F32) return EA_ERR_UNSUPPORTED;
+  if (s->head_dim != 64 && s->head_dim != 128) return EA_ERR_UNSUPPORTED;
+  if (s->seqlen > MAX_SEQLEN) return EA_ERR_UNSUPPORTED;
+  if (!std::isfinite(p->alpha) || !(p->alpha > 1.0f)) return EA_ERR_INVALID_ARG;
+  if (!std::isfinite(p->scale) || !(p->scale > 0.0f)) return EA_ERR_INVALID_ARG;
+  if (p->causal != 0 && p->causal != 1) return EA_ERR_INVALID_ARG;
+  if (p->need_bwd != 0 && p->need_bwd != 1) return EA_ERR_INVALID_ARG;
+  if (p->max_iter < 0 || p->max_iter > MAX_ITER_CAP) return EA_ERR_INVALID_ARG;
+  if (!std::isfinite(p->tol) || p->tol < 0.0f) return EA_ERR_INVALID_ARG;
+  const int64_t BH = (int64_t)s->batch * s->heads;
+  const int64_t n = s->seqlen;
+  const int64_t T = (n + 63) / 64;
+  // grid sizes and in-kernel offsets use 32-bit block counts
+  if (BH * ((n + 63) / 64) > (int64_t)INT32_MAX / 2) return EA_ERR_UNSUPPORTED;
+  out->BH = BH;
+  out->n = n;
+  out->d = s->head_dim;
+  out->T = T;
+  out->elems = BH * n * s->head_dim;
+  out->dtype = s->dtype;
+  out->esize = s->dtype == EA_BF16 ? 2 : 4;
+  return EA_OK;
+}
+
+void fill_sizes(const Dims& d, ea_sizes* z) {
+  z->tau = (size_t)(d.BH * d.n) * 4;
+  z->o2 = (size_t)d.elems * 4;
+  z->block_mask = (size_t)(d.BH * d.T * d.T);
+  z->q_count = (size_t)(d.BH * d.T) * 4;
+  z->q_index = (size_t)(d.BH * d.T * d.T) * 4;
+  z->k_count = z->q_count;
+  z->k_index = z->q_index;
+  z->stats = (size_t)(d.BH * ((d.n + 127) / 128)) * 4;
+  z->ws_fwd = 0;
+  z->ws_bwd = (size_t)(d.BH * d.n) * 4;
+}
+
+bool tensor_ok(const void* p) { return p && aligned(p, 16); }
+bool small_ok(const void* p) { return p && aligned(p, 4); }
+
+ea_status check_tables(const ea_residuals* r) {
+  if (!r) return EA_ERR_INVALID_ARG;
+  if (!small_ok(r->tau) || !r->block_mask || !small_ok(r->q_count) || !small_ok(r->q_index) ||
+      !small_ok(r->k_count) || !small_ok(r->k_index))
+    return EA_ERR_INVALID_ARG;
+  if (r->stats && !aligned(r->stats, 4)) return EA_ERR_INVALID_ARG;
+  return EA_OK;
+}
+
+ea_status from_hip(hipError_t e) { return e == hipSuccess ? EA_OK : EA_ERR_HIP; }
+
+}  // namespace
+}  // namespace ea
+
+using namespace ea;
+
+extern "C" {
+
+void entmax_attn_default_params(ea_params* p) {
+  if (!p) return;
+  p->alpha = 1.5f;
+  p->scale = 0.125f;
+  p->causal = 0;
+  p->max_iter = DEFAULT_MAX_ITER;
+  p->tol = DEFAULT_TOL;
+  p->need_bwd = 1;
+}
+
+ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_sizes* out) {
+  Dims d;
+  ea_status st = check_shape(shape, params, &d);
+  if (st != EA_OK) return st;
+  if (!out) return EA_ERR_INVALID_ARG;
+  fill_sizes(d, out);
+  return EA_OK;
+}
+
+ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const void* q,
+                          const void* k, const void* v, void* o, const ea_residuals* res,
+                          void* workspace, size_t ws_bytes, void* stream) {
+  (void)workspace;
+  (void)ws_bytes;
+  Dims d;
+  ea_status st = check_shape(shape, params, &d);
+  if (st != EA_OK) return st;
+  if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(o)) return EA_ERR_INVALID_ARG;
+  if ((st = check_tables(res)) != EA_OK) return st;
+  if (params->need_bwd && !tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float c = (params->alpha - 1.0f) * params->scale;
+  const float gamma = 1.0f / (params->alpha - 1.0f);
+  const int gk = gamma_kind(params->alpha);
+
+  TauArgs ta{q, k, res->tau, res->block_mask, res->stats, (int)d.BH, (int)d.n, (int)d.T,
+             c, params->alpha, gamma, params->causal, params->max_iter, params->tol, gk};
+  if ((st = from_hip(launch_tau(ta, d.dtype, (int)d.d, s))) != EA_OK) return st;
+
+  CompactArgs ca{res->block_mask, res->q_count, res->q_index, res->k_count, res->k_index,
+                 (int)d.BH, (int)d.T};
+  if ((st = from_hip(launch_compact(ca, s))) != EA_OK) return st;
+
+  FwdArgs fa{q, k, v, o, params->need_bwd ? res->o2 : nullptr, res->tau, res->q_count,
+             res->q_index, (int)d.BH, (int)d.n, (int)d.T, c, gamma, params->causal, gk};
+  return from_hip(launch_fwd(fa, d.dtype, (int)d.d, params->need_bwd != 0, s));
+}
+
+ea_status entmax_attn_bwd(const ea_shape* shape, const ea_params* params, const void* q,
+                          const void* k, const void* v, const void* dout,
+                          const ea_residuals* res, float* dq, float* dk, float* dv,
+                          void* workspace, size_t ws_bytes, void* stream) {
+  Dims d;
+  ea_status st = check_shape(shape, params, &d);
+  if (st != EA_OK) return st;
+  if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(dout)) return EA_ERR_INVALID_ARG;
+  if (!tensor_ok(dq) || !tensor_ok(dk) || !tensor_ok(dv)) return EA_ERR_INVALID_ARG;
+  if ((st = check_tables(res)) != EA_OK) return st;
+  if (!tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
+  ea_sizes z;
+  fill_sizes(d, &z);
+  if (!workspace || !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
+  if (ws_bytes < z.ws_bwd) return EA_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float c = (params->alpha - 1.0f) * params->scale;
+  const float gamma = 1.0f / (params->alpha - 1.0f);
+  float* delta = static_cast<float*>(workspace);
+
+  DeltaArgs da{dout, res->o2, delta, d.BH * d.n};
+  if ((st = from_hip(launch_delta(da, d.dtype, (int)d.d, s))) != EA_OK) return st;
+
+  BwdArgs ba{q, k, v, dout, res->tau, delta, res->q_count, res->q_index, res->k_count,
+             res->k_index, dq, dk, dv, (int)d.BH, (int)d.n, (int)d.T, c, gamma,
+             params->scale, params->causal, gamma_kind(params->alpha)};
+  if ((st = from_hip(launch_bwd_dkdv(ba, d.dtype, (int)d.d, s))) != EA_OK) return st;
+  return from_hip(launch_bwd_dq(ba, d.dtype, (int)d.d, s));
+}
+
+const char* entmax_attn_status_string(ea_status s) {
+  switch (s) {
+    case EA_OK: return "ok";
+    case EA_ERR_INVALID_ARG: return "invalid argument";
+    case EA_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case EA_ERR_WORKSPACE: return "workspace too small";
+    case EA_ERR_HIP: return "HIP launch failure";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

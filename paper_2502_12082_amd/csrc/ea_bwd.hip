@@ -1,0 +1,344 @@
+// ea_bwd.hip -- sparse alpha-entmax attention backward.
+//
+// With tau from the forward, u_ij = [x_ij - tau_i]_+^(gamma-1) on the support
+// (= p^(2-alpha), the sparse Jacobian Diag(u) - u u^T / |u|_1 of Sec. 3.2.2)
+// and O2 saved by the forward (App. A.2):
+//   delta_i = <dO_i, O2_i>                                   (App. A.2)
+//   dP_ij   = <dO_i, v_j>,  dS_ij = u_ij (dP_ij - delta_i)    (App. A.2)
+//   dV_j = sum_{i in K_j} P_ij^T dO_i                         (Eq. 13)
+//   dK_j = scale * sum_{i in K_j} dS_ij^T q_i                 (Eq. 12)
+//   dQ_i = scale * sum_{j in Q_i} dS_ij k_j                   (Eq. 11)
+// split into a delta pre-kernel, a dK/dV kernel over key blocks and a dQ
+// kernel over query blocks (Algorithms 4 and 5, visiting only the blocks of
+// the lookup tables as in App. A.5).  `scale` appears because the entmax
+// input is scale * Q K^T; no alpha factor survives the chain rule.
+//
+// Precision: S and dP are bf16 x bf16 products accumulated in fp32; P is
+// rounded to bf16 for P^T dO; dS is fed to the MFMA as a two-term bf16 split
+// (hi + lo) so dK and dQ keep ~16 mantissa bits of dS; outputs are fp32.
+//
+// gfx950 layout: 2 waves per workgroup, 32 resident rows per wave in
+// registers (K and V rows for dK/dV; Q and dO rows for dQ), the other side's
+// 64-row tiles staged in LDS row-major (for S, dP) and transposed (for the
+// permuted contraction of P^T dO, dS^T Q, dS K).  No atomics: every output
+// row has one owner, so results are deterministic.
+#include "ea_common.h"
+#include "ea_internal.h"
+
+namespace ea {
+
+namespace {
+
+constexpr int BWD_NT = 128;
+
+// ------------------------------------------------------------------ delta
+
+template <typename E, int D>
+__global__ __launch_bounds__(256) void delta_kernel(DeltaArgs a) {
+  constexpr int PER = D / 16;  // 16 lanes per row
+  const long long row = (long long)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int sl = threadIdx.x & 15;
+  float acc = 0.f;
+  if (row < a.rows) {
+    const E* dO = static_cast<const E*>(a.dout) + row * D + sl * PER;
+    const float* o2 = a.o2 + row * D + sl * PER;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc = fmaf((float)dO[e], o2[e], acc);
+  }
+#pragma unroll
+  for (int m = 8; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+  if (row < a.rows && sl == 0) a.delta[row] = acc;
+}
+
+// ------------------------------------------------------------------ dK dV
+
+template <typename E, int D, int GK>
+__global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
+  using G = TileGeom<E, D>;
+  using M = Mma<E>;
+  constexpr int KS = D / M::KW;
+  constexpr int NTD = D / 32;
+  constexpr int PS = perm_steps<E>();
+  __shared__ __attribute__((aligned(16))) E q_rm[G::RM_ELEMS];
+  __shared__ __attribute__((aligned(16))) E q_tr[G::TR_ELEMS];
+  __shared__ __attribute__((aligned(16))) E do_rm[G::RM_ELEMS];
+  __shared__ __attribute__((aligned(16))) E do_tr[G::TR_ELEMS];
+  __shared__ float tau_s[BLK], del_s[BLK];
+
+  const int lane = lane_id(), w = wave_id();
+  const int n = a.n, T = a.T;
+  const int bh = blockIdx.x % a.BH;
+  const int kb = blockIdx.x / a.BH;  // causal: small kb has the longest list
+  const int k0 = kb * BLK + 32 * w;
+  const int j = k0 + (lane & 31);
+  const bool wave_ok = k0 < n;
+  const size_t head = (size_t)bh * n * D;
+  const E* Qg = static_cast<const E*>(a.q) + head;
+  const E* Kg = static_cast<const E*>(a.k) + head;
+  const E* Vg = static_cast<const E*>(a.v) + head;
+  const E* dOg = static_cast<const E*>(a.dout) + head;
+  const float* taug = a.tau + (size_t)bh * n;
+  const float* delg = a.delta + (size_t)bh * n;
+  const float c = a.c, g = a.gamma;
+
+  typename M::frag kf[KS], vf[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    kf[kk] = load_row_frag_global<E, D>(Kg, j, n, kk);
+    vf[kk] = load_row_frag_global<E, D>(Vg, j, n, kk);
+  }
+
+  const int32_t* list = a.k_index + ((size_t)bh * T + kb) * T;
+  const int cnt = a.k_count[(size_t)bh * T + kb];
+
+  f32x16 dk[NTD], dv[NTD];
+#pragma unroll
+  for (int t = 0; t < NTD; ++t) {
+    dk[t] = zero16();
+    dv[t] = zero16();
+  }
+
+  TileRegs<E, D, BWD_NT> qr, dr;
+  float tv = 0.f, dlv = 0.f;
+  auto prefetch = [&](int qb) {
+    qr.load(Qg, qb * BLK, n);
+    dr.load(dOg, qb * BLK, n);
+    if (threadIdx.x < BLK) {
+      const int r = qb * BLK + threadIdx.x;
+      tv = r < n ? taug[r] : 0.f;
+      dlv = r < n ? delg[r] : 0.f;
+    }
+  };
+  if (cnt > 0) prefetch(list[0]);
+  for (int e = 0; e < cnt; ++e) {
+    const int qb = list[e];
+    __syncthreads();
+    qr.store_rm(q_rm);
+    qr.store_tr(q_tr);
+    dr.store_rm(do_rm);
+    dr.store_tr(do_tr);
+    if (threadIdx.x < BLK) {
+      tau_s[threadIdx.x] = tv;
+      del_s[threadIdx.x] = dlv;
+    }
+    __syncthreads();
+    if (e + 1 < cnt) prefetch(list[e + 1]);
+    if (!wave_ok) continue;
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh) {
+      const int i0 = qb * BLK + 32 * qh;
+      if (i0 >= n || (a.causal && k0 > i0 + 31)) continue;
+      const bool edge = i0 + 31 >= n || k0 + 31 >= n || (a.causal && k0 + 31 > i0);
+      // S = Q K^T and dP = dO V^T, rows = queries, columns = this wave's keys
+      f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        s = M::mma(lds_row_frag<E, D>(q_rm, 32 * qh + (lane & 31), kk), kf[kk], s);
+        dp = M::mma(lds_row_frag<E, D>(do_rm, 32 * qh + (lane & 31), kk), vf[kk], dp);
+      }
+      float p[16], ds[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int qi = 32 * qh + crow(r);
+        float zp = relu_z(c, s[r], tau_s[qi]);
+        if (edge) {
+          const int i = qb * BLK + qi;
+          if (i >= n || j >= n || (a.causal && j > i)) zp = 0.f;
+        }
+        float u;
+        Gamma<GK>::pu(zp, g, p[r], u);
+        ds[r] = u * (dp[r] - del_s[qi]);
+      }
+#pragma unroll
+      for (int t = 0; t < PS; ++t) {
+        const typename M::frag pa = M::pack(p, t);
+        typename M::frag dh, dl;
+        M::pack_split(ds, t, dh, dl);
+#pragma unroll
+        for (int nt = 0; nt < NTD; ++nt) {
+          const int col = 32 * nt + (lane & 31);
+          dv[nt] = M::mma(pa, lds_perm_frag<E>(do_tr, col, 32 * qh, t), dv[nt]);
+          const typename M::frag qb_ = lds_perm_frag<E>(q_tr, col, 32 * qh, t);
+          dk[nt] = M::mma(dh, qb_, dk[nt]);
+          if constexpr (!M::exact_operands) dk[nt] = M::mma(dl, qb_, dk[nt]);
+        }
+      }
+    }
+  }
+
+  if (!wave_ok) return;
+  float* dK = a.dk + head;
+  float* dV = a.dv + head;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int key = k0 + crow(r);
+    if (key < n) {
+#pragma unroll
+      for (int nt = 0; nt < NTD; ++nt) {
+        const size_t off = (size_t)key * D + 32 * nt + (lane & 31);
+        dK[off] = a.scale * dk[nt][r];
+        dV[off] = dv[nt][r];
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------------- dQ
+
+template <typename E, int D, int GK>
+__global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
+  using G = TileGeom<E, D>;
+  using M = Mma<E>;
+  constexpr int KS = D / M::KW;
+  constexpr int NTD = D / 32;
+  constexpr int PS = perm_steps<E>();
+  __shared__ __attribute__((aligned(16))) E k_rm[G::RM_ELEMS];
+  __shared__ __attribute__((aligned(16))) E k_tr[G::TR_ELEMS];
+  __shared__ __attribute__((aligned(16))) E v_rm[G::RM_ELEMS];
+
+  const int lane = lane_id(), w = wave_id();
+  const int n = a.n, T = a.T;
+  const int bh = blockIdx.x % a.BH;
+  int qb = blockIdx.x / a.BH;
+  if (a.causal) qb = T - 1 - qb;  // longest lists first
+  const int q0 = qb * BLK + 32 * w;
+  const int i = q0 + (lane & 31);
+  const bool wave_ok = q0 < n;
+  const size_t head = (size_t)bh * n * D;
+  const E* Qg = static_cast<const E*>(a.q) + head;
+  const E* Kg = static_cast<const E*>(a.k) + head;
+  const E* Vg = static_cast<const E*>(a.v) + head;
+  const E* dOg = static_cast<const E*>(a.dout) + head;
+  const float tau = i < n ? a.tau[(size_t)bh * n + i] : 0.f;
+  const float del = i < n ? a.delta[(size_t)bh * n + i] : 0.f;
+  const float c = a.c, g = a.gamma;
+
+  typename M::frag qf[KS], df[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    qf[kk] = load_row_frag_global<E, D>(Qg, i, n, kk);
+    df[kk] = load_row_frag_global<E, D>(dOg, i, n, kk);
+  }
+
+  const int32_t* list = a.q_index + ((size_t)bh * T + qb) * T;
+  const int cnt = a.q_count[(size_t)bh * T + qb];
+
+  f32x16 dq[NTD];
+#pragma unroll
+  for (int t = 0; t < NTD; ++t) dq[t] = zero16();
+
+  TileRegs<E, D, BWD_NT> kr, vr;
+  if (cnt > 0) {
+    kr.load(Kg, list[0] * BLK, n);
+    vr.load(Vg, list[0] * BLK, n);
+  }
+  for (int e = 0; e < cnt; ++e) {
+    const int kb = list[e];
+    __syncthreads();
+    kr.store_rm(k_rm);
+    kr.store_tr(k_tr);
+    vr.store_rm(v_rm);
+    __syncthreads();
+    if (e + 1 < cnt) {
+      kr.load(Kg, list[e + 1] * BLK, n);
+      vr.load(Vg, list[e + 1] * BLK, n);
+    }
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const int j0 = kb * BLK + 32 * sub;
+      if (!wave_ok || j0 >= n || (a.causal && j0 > min(n - 1, q0 + 31))) continue;
+      const bool edge = j0 + 31 >= n || (a.causal && j0 + 31 > q0);
+      // S^T = K Q^T and dP^T = V dO^T: rows = keys, columns = this wave's queries
+      f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        s = M::mma(lds_row_frag<E, D>(k_rm, 32 * sub + (lane & 31), kk), qf[kk], s);
+        dp = M::mma(lds_row_frag<E, D>(v_rm, 32 * sub + (lane & 31), kk), df[kk], dp);
+      }
+      float ds[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float zp = relu_z(c, s[r], tau);
+        if (edge) {
+          const int jj = j0 + crow(r);
+          if (jj >= n || (a.causal && jj > i)) zp = 0.f;
+        }
+        float p, u;
+        Gamma<GK>::pu(zp, g, p, u);
+        ds[r] = u * (dp[r] - del);
+      }
+#pragma unroll
+      for (int t = 0; t < PS; ++t) {
+        typename M::frag dh, dl;
+        M::pack_split(ds, t, dh, dl);
+#pragma unroll
+        for (int nt = 0; nt < NTD; ++nt) {
+          const typename M::frag kb_ = lds_perm_frag<E>(k_tr, 32 * nt + (lane & 31), 32 * sub, t);
+          dq[nt] = M::mma(dh, kb_, dq[nt]);
+          if constexpr (!M::exact_operands) dq[nt] = M::mma(dl, kb_, dq[nt]);
+        }
+      }
+    }
+  }
+
+  if (!wave_ok) return;
+  float* dQ = a.dq + head;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int ir = q0 + crow(r);
+    if (ir < n) {
+#pragma unroll
+      for (int nt = 0; nt < NTD; ++nt) dQ[(size_t)ir * D + 32 * nt + (lane & 31)] = a.scale * dq[nt][r];
+    }
+  }
+}
+
+template <typename E, int D>
+hipError_t launch_dkdv_d(const BwdArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)(a.BH * a.T)), block(BWD_NT);
+  switch (a.gk) {
+    case 1: hipLaunchKernelGGL((dkdv_kernel<E, D, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((dkdv_kernel<E, D, 2>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((dkdv_kernel<E, D, 4>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((dkdv_kernel<E, D, 0>), grid, block, 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename E, int D>
+hipError_t launch_dq_d(const BwdArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)(a.BH * a.T)), block(BWD_NT);
+  switch (a.gk) {
+    case 1: hipLaunchKernelGGL((dq_kernel<E, D, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((dq_kernel<E, D, 2>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((dq_kernel<E, D, 4>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((dq_kernel<E, D, 0>), grid, block, 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename E, int D>
+hipError_t launch_delta_d(const DeltaArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)((a.rows + 15) / 16)), block(256);
+  hipLaunchKernelGGL((delta_kernel<E, D>), grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_delta(const DeltaArgs& a, int dtype, int head_dim, hipStream_t s) {
+  if (dtype == 0) return head_dim == 64 ? launch_delta_d<__bf16, 64>(a, s) : launch_delta_d<__bf16, 128>(a, s);
+  return head_dim == 64 ? launch_delta_d<float, 64>(a, s) : launch_delta_d<float, 128>(a, s);
+}
+
+hipError_t launch_bwd_dkdv(const BwdArgs& a, int dtype, int head_dim, hipStream_t s) {
+  if (dtype == 0) return head_dim == 64 ? launch_dkdv_d<__bf16, 64>(a, s) : launch_dkdv_d<__bf16, 128>(a, s);
+  return head_dim == 64 ? launch_dkdv_d<float, 64>(a, s) : launch_dkdv_d<float, 128>(a, s);
+}
+
+hipError_t launch_bwd_dq(const BwdArgs& a, int dtype, int head_dim, hipStream_t s) {
+  if (dtype == 0) return head_dim == 64 ? launch_dq_d<__bf16, 64>(a, s) : launch_dq_d<__bf16, 128>(a, s);
+  return head_dim == 64 ? launch_dq_d<float, 64>(a, s) : launch_dq_d<float, 128>(a, s);
+}
+
+}  // namespace ea

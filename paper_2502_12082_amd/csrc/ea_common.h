@@ -1,0 +1,289 @@
+// ea_common.h -- device building blocks shared by the alpha-entmax attention
+// kernels for gfx950 (CDNA4): MFMA traits for bf16 and fp32 operands, register
+// fragment loaders, 64-row LDS tiles (row-major and transposed), and the
+// per-element alpha-entmax maps specialised on gamma = 1/(alpha-1).
+//
+// Conventions used by every kernel
+// --------------------------------
+// * Tensors are [B*H, n, D] row-major, D in {64, 128}; blocks are 64 rows.
+// * One wave owns a 32-row slab of the "resident" side of a product and
+//   computes 32x32 output tiles with v_mfma_f32_32x32x16_bf16 (bf16 inputs) or
+//   v_mfma_f32_32x32x2_f32 (fp32 inputs), fp32 accumulation.
+// * Accumulator layout of a 32x32 tile (identical for both instructions):
+//   value r (0..15) of lane l sits at row 8*(r/4) + 4*(l/32) + (r%4), column
+//   l%32.  `crow(r)` returns that row for the calling lane.
+// * A and B operands: lane l supplies row (A) or column (B) l%32 and the
+//   k-slice [8*(l/32), 8*(l/32)+8) of a 16-wide k step (bf16), or k = l/32 of
+//   a 2-wide k step (fp32).
+// * Probability tiles are fed back to the MFMA straight from the accumulator
+//   registers: the contraction index is permuted (the same permutation on both
+//   operands), so step t of a 32-wide contraction uses accumulator values
+//   [8t, 8t+8) (bf16) or value t (fp32); `perm_key` gives the contraction row
+//   that a lane's slot maps to, and the transposed LDS tiles are read with the
+//   same permutation.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ea {
+
+constexpr int BLK = 64;  // mask block edge (rows and columns)
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+// Row of accumulator value r for the calling lane (see the layout note above).
+__device__ __forceinline__ int crow(int r) { return 8 * (r >> 2) + 4 * (lane_id() >> 5) + (r & 3); }
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+// ------------------------------------------------------------ MFMA traits
+
+template <typename E>
+struct Mma;
+
+template <>
+struct Mma<__bf16> {
+  using frag = bf16x8;
+  static constexpr int KW = 16;   // contraction width of one instruction
+  static constexpr int EPL = 8;   // operand elements per lane
+  __device__ __forceinline__ static f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  // A operand from accumulator values [8t, 8t+8), rounded to nearest even.
+  __device__ __forceinline__ static frag pack(const float* v, int t) {
+    frag f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = (__bf16)v[8 * t + e];
+    return f;
+  }
+  // Two-term split v ~ hi + lo, both bf16; hi + lo carries ~16 mantissa bits.
+  __device__ __forceinline__ static void pack_split(const float* v, int t, frag& hi, frag& lo) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      __bf16 h = (__bf16)v[8 * t + e];
+      hi[e] = h;
+      lo[e] = (__bf16)(v[8 * t + e] - (float)h);
+    }
+  }
+  static constexpr bool exact_operands = false;
+};
+
+template <>
+struct Mma<float> {
+  using frag = float;
+  static constexpr int KW = 2;
+  static constexpr int EPL = 1;
+  __device__ __forceinline__ static f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ __forceinline__ static frag pack(const float* v, int t) { return v[t]; }
+  __device__ __forceinline__ static void pack_split(const float* v, int t, frag& hi, frag& lo) {
+    hi = v[t];
+    lo = 0.f;
+  }
+  static constexpr bool exact_operands = true;  // fp32 operands need no split
+};
+
+// Steps of a 32-wide contraction fed from accumulator registers.
+template <typename E>
+constexpr int perm_steps() { return 32 / Mma<E>::KW; }
+
+// Contraction row (0..31) that slot (step t, element e) of the calling lane
+// holds, under the permutation described at the top of this file.
+template <typename E>
+__device__ __forceinline__ int perm_key(int t, int e) {
+  const int h = lane_id() >> 5;
+  if constexpr (Mma<E>::EPL == 8) {
+    return 8 * (2 * t + (e >> 2)) + 4 * h + (e & 3);
+  } else {
+    return 8 * (t >> 2) + 4 * h + (t & 3);
+  }
+}
+
+// ------------------------------------------------------- global fragments
+
+// Row fragment for k step kk of row `row` of a [*, D] row-major global
+// matrix: bf16 -> 8 values at k = 16kk + 8h; fp32 -> 1 value at k = 2kk + h.
+// Rows outside [0, nrows) read as zero.
+template <typename E, int D>
+__device__ __forceinline__ typename Mma<E>::frag load_row_frag_global(const E* base, int row,
+                                                                      int nrows, int kk) {
+  const int h = lane_id() >> 5;
+  if constexpr (Mma<E>::EPL == 8) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row < nrows) v = *reinterpret_cast<const u32x4*>(base + (size_t)row * D + 16 * kk + 8 * h);
+    return __builtin_bit_cast(bf16x8, v);
+  } else {
+    float v = 0.f;
+    if (row < nrows) v = base[(size_t)row * D + 2 * kk + h];
+    return v;
+  }
+}
+
+// -------------------------------------------------------------- LDS tiles
+//
+// A 64 x D tile of a [*, D] row-major global matrix, staged in LDS in up to
+// two layouts:
+//   row-major   rm[r * RP + c]            RP = D + 16 bytes of padding
+//   transposed  tr[c * 64 + swz(c, r)]    r = tile row, XOR-swizzled in groups
+//                                         of 4 so that both the transposing
+//                                         stores and the 8-byte permuted reads
+//                                         spread over the LDS banks.
+// Loading goes through registers (16-byte global loads, consecutive threads
+// on consecutive 16-byte chunks of a row) so the next tile can be in flight
+// while the current one is consumed.
+
+template <typename E, int D>
+struct TileGeom {
+  static constexpr int VEC = 16 / (int)sizeof(E);        // elements per 16-byte chunk
+  static constexpr int CPR = D / VEC;                    // chunks per row
+  static constexpr int CHUNKS = BLK * CPR;               // chunks per tile
+  static constexpr int RP = D + VEC;                     // row-major pitch (elements)
+  static constexpr int RM_ELEMS = BLK * RP;
+  static constexpr int TR_ELEMS = D * BLK;
+};
+
+__device__ __forceinline__ int tr_swz(int c, int r) {
+  return r ^ ((((c ^ (c >> 3)) & 15)) << 2);
+}
+
+template <typename E, int D, int NT>
+struct TileRegs {
+  static constexpr int PER = TileGeom<E, D>::CHUNKS / NT;
+  static_assert(TileGeom<E, D>::CHUNKS % NT == 0, "tile chunks must divide the workgroup");
+  u32x4 v[PER];
+
+  // Load tile rows [row0, row0 + 64) of a matrix with `nrows` rows; rows past
+  // the end are zero.
+  __device__ __forceinline__ void load(const E* base, int row0, int nrows) {
+    constexpr int CPR = TileGeom<E, D>::CPR, VEC = TileGeom<E, D>::VEC;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = threadIdx.x + NT * i;
+      const int r = q / CPR, c = q % CPR;
+      const int row = row0 + r;
+      u32x4 x = {0u, 0u, 0u, 0u};
+      if (row < nrows) x = *reinterpret_cast<const u32x4*>(base + (size_t)row * D + c * VEC);
+      v[i] = x;
+    }
+  }
+
+  __device__ __forceinline__ void store_rm(E* rm) const {
+    constexpr int CPR = TileGeom<E, D>::CPR, VEC = TileGeom<E, D>::VEC, RP = TileGeom<E, D>::RP;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = threadIdx.x + NT * i;
+      const int r = q / CPR, c = q % CPR;
+      *reinterpret_cast<u32x4*>(rm + r * RP + c * VEC) = v[i];
+    }
+  }
+
+  __device__ __forceinline__ void store_tr(E* tr) const {
+    constexpr int CPR = TileGeom<E, D>::CPR, VEC = TileGeom<E, D>::VEC;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = threadIdx.x + NT * i;
+      const int r = q / CPR, c0 = (q % CPR) * VEC;
+      if constexpr (sizeof(E) == 2) {
+        const uint16_t* s = reinterpret_cast<const uint16_t*>(&v[i]);
+        uint16_t* t = reinterpret_cast<uint16_t*>(tr);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) t[(c0 + e) * BLK + tr_swz(c0 + e, r)] = s[e];
+      } else {
+        const float* s = reinterpret_cast<const float*>(&v[i]);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) tr[(c0 + e) * BLK + tr_swz(c0 + e, r)] = s[e];
+      }
+    }
+  }
+};
+
+// A-operand row fragment from a row-major LDS tile: tile row `r`, k step kk.
+template <typename E, int D>
+__device__ __forceinline__ typename Mma<E>::frag lds_row_frag(const E* rm, int r, int kk) {
+  constexpr int RP = TileGeom<E, D>::RP;
+  const int h = lane_id() >> 5;
+  if constexpr (Mma<E>::EPL == 8) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(rm + r * RP + 16 * kk + 8 * h));
+  } else {
+    return rm[r * RP + 2 * kk + h];
+  }
+}
+
+// B-operand fragment for the permuted contraction over tile rows
+// [rbase, rbase + 32): column `c` of the tile (an index in 0..D-1), step t.
+template <typename E>
+__device__ __forceinline__ typename Mma<E>::frag lds_perm_frag(const E* tr, int c, int rbase, int t) {
+  const int h = lane_id() >> 5;
+  if constexpr (Mma<E>::EPL == 8) {
+    const int r0 = rbase + 16 * t + 4 * h;  // rows r0..r0+3 and r0+8..r0+11
+    const E* col = tr + c * BLK;
+    u32x2 a = *reinterpret_cast<const u32x2*>(col + tr_swz(c, r0));
+    u32x2 b = *reinterpret_cast<const u32x2*>(col + tr_swz(c, r0 + 8));
+    u32x4 v = {a.x, a.y, b.x, b.y};
+    return __builtin_bit_cast(bf16x8, v);
+  } else {
+    const int r = rbase + 8 * (t >> 2) + 4 * h + (t & 3);
+    return tr[c * BLK + tr_swz(c, r)];
+  }
+}
+
+// ------------------------------------------------- per-element entmax maps
+//
+// zp = clamp(x - tau, 0, 1) where x = c * s; within the bracket of Algorithm 1
+// (tau >= max_j x_j - 1) every z = x - tau is <= 1, so the clamp is exactly
+// [z]_+ and folds into one v_fma_f32 with the clamp bit.
+__device__ __forceinline__ float relu_z(float c, float s, float tau) {
+  return __builtin_amdgcn_fmed3f(fmaf(c, s, -tau), 0.f, 1.f);
+}
+
+// GK = gamma for the integer cases 1 (alpha = 2), 2 (alpha = 1.5),
+// 4 (alpha = 1.25); GK = 0 is any alpha > 1 via exp2/log2.
+template <int GK>
+struct Gamma {
+  // p = zp^gamma and u = zp^(gamma-1) on the strict support zp > 0.
+  __device__ __forceinline__ static void pu(float zp, float g, float& p, float& u) {
+    if constexpr (GK == 1) {
+      p = zp;
+      u = zp > 0.f ? 1.f : 0.f;
+    } else if constexpr (GK == 2) {
+      p = zp * zp;
+      u = zp;
+    } else if constexpr (GK == 4) {
+      const float z2 = zp * zp;
+      u = z2 * zp;
+      p = z2 * z2;
+    } else {
+      const float l = __log2f(zp);
+      p = zp > 0.f ? exp2f(g * l) : 0.f;
+      u = zp > 0.f ? exp2f((g - 1.f) * l) : 0.f;
+    }
+  }
+  __device__ __forceinline__ static float p_only(float zp, float g) {
+    if constexpr (GK == 1) {
+      return zp;
+    } else if constexpr (GK == 2) {
+      return zp * zp;
+    } else if constexpr (GK == 4) {
+      const float z2 = zp * zp;
+      return z2 * z2;
+    } else {
+      return zp > 0.f ? exp2f(g * __log2f(zp)) : 0.f;
+    }
+  }
+};
+
+}  // namespace ea

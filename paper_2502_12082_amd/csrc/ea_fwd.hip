@@ -1,0 +1,211 @@
+// ea_fwd.hip -- block-mask compaction and the sparse alpha-entmax forward.
+//
+// Compaction (Sec. 3.2.1, "pointer-increment lookup tables"; App. A.5): from
+// the block mask M, Q_i = {j : M_ij = 1} for every query block i and
+// K_j = {i : M_ij = 1} for every key block j, each list ascending.  Stored as
+// a count per block plus a fixed-stride index row of T entries.
+//
+// Forward (Algorithm 2 with the masked loop of App. A.5): for every query
+// block i and every key block j in Q_i, recompute S = Q_i K_j^T, P =
+// [(alpha-1) S - tau]_+^gamma (Eq. 2) and accumulate O_i += P V_j.  When a
+// backward will follow, also accumulate U V_j and sum U with
+// U = [(alpha-1) S - tau]_+^(gamma-1) on the support, and write
+// O2_i = U V / sum U (the O^(2) of App. A.2).  O is not renormalised: the
+// row sums are 1 + f(tau) of the returned tau (Algorithm 1 output).
+//
+// gfx950 layout: one workgroup = 2 waves = one 64-row query block; each wave
+// holds 32 query rows as MFMA B operands, computes S^T (keys x queries) so the
+// probabilities come out with one query per lane, and feeds them back as the
+// A operand of P V with a permuted contraction order (see ea_common.h).  K is
+// staged row-major and V transposed in LDS; the next listed block is loaded
+// into registers while the current one is consumed.
+#include "ea_common.h"
+#include "ea_internal.h"
+
+namespace ea {
+
+namespace {
+
+// ------------------------------------------------------------ compaction
+
+constexpr int CMP_NT = 256;
+
+__global__ __launch_bounds__(CMP_NT) void compact_kernel(CompactArgs a) {
+  const int lane = lane_id();
+  const long long gw = (long long)blockIdx.x * (CMP_NT / 64) + wave_id();
+  const long long rows = (long long)a.BH * a.T;
+  if (gw >= 2 * rows) return;
+  const bool by_col = gw >= rows;
+  const long long idx = by_col ? gw - rows : gw;
+  const int bh = (int)(idx / a.T), r = (int)(idx % a.T);
+  const int T = a.T;
+  const uint8_t* M = a.mask + (size_t)bh * T * T;
+  int32_t* out = (by_col ? a.k_index : a.q_index) + ((size_t)bh * T + r) * T;
+  int base = 0;
+  for (int c0 = 0; c0 < T; c0 += 64) {
+    const int cidx = c0 + lane;
+    bool bit = false;
+    if (cidx < T) bit = (by_col ? M[(size_t)cidx * T + r] : M[(size_t)r * T + cidx]) != 0;
+    const unsigned long long b = __ballot(bit);
+    const int pre = __builtin_amdgcn_mbcnt_hi((unsigned)(b >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)b, 0u));
+    if (bit) out[base + pre] = cidx;
+    base += __popcll(b);
+  }
+  if (lane == 0) (by_col ? a.k_count : a.q_count)[(size_t)bh * T + r] = base;
+}
+
+// --------------------------------------------------------------- forward
+
+constexpr int FWD_NT = 128;
+
+template <typename E, int D, int GK, bool TRAIN>
+__global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
+  using G = TileGeom<E, D>;
+  using M = Mma<E>;
+  constexpr int KS = D / M::KW;
+  constexpr int NTD = D / 32;
+  constexpr int PS = perm_steps<E>();
+  __shared__ __attribute__((aligned(16))) E k_rm[G::RM_ELEMS];
+  __shared__ __attribute__((aligned(16))) E v_tr[G::TR_ELEMS];
+
+  const int lane = lane_id(), w = wave_id();
+  const int n = a.n, T = a.T;
+  const int bh = blockIdx.x % a.BH;
+  int qb = blockIdx.x / a.BH;
+  if (a.causal) qb = T - 1 - qb;  // longest lists first
+  const int q0 = qb * BLK + 32 * w;
+  const int i = q0 + (lane & 31);
+  const bool wave_ok = q0 < n;
+  const size_t head = (size_t)bh * n * D;
+  const E* Q = static_cast<const E*>(a.q) + head;
+  const E* K = static_cast<const E*>(a.k) + head;
+  const E* V = static_cast<const E*>(a.v) + head;
+  const float tau = i < n ? a.tau[(size_t)bh * n + i] : 0.f;
+  const float c = a.c, g = a.gamma;
+
+  typename M::frag qf[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) qf[kk] = load_row_frag_global<E, D>(Q, i, n, kk);
+
+  const int32_t* list = a.q_index + ((size_t)bh * T + qb) * T;
+  const int cnt = a.q_count[(size_t)bh * T + qb];
+
+  f32x16 o[NTD], o2[NTD];
+#pragma unroll
+  for (int t = 0; t < NTD; ++t) {
+    o[t] = zero16();
+    o2[t] = zero16();
+  }
+  float usum = 0.f;
+
+  TileRegs<E, D, FWD_NT> kr, vr;
+  if (cnt > 0) {
+    kr.load(K, list[0] * BLK, n);
+    vr.load(V, list[0] * BLK, n);
+  }
+  for (int e = 0; e < cnt; ++e) {
+    const int kb = list[e];
+    __syncthreads();
+    kr.store_rm(k_rm);
+    vr.store_tr(v_tr);
+    __syncthreads();
+    if (e + 1 < cnt) {
+      kr.load(K, list[e + 1] * BLK, n);
+      vr.load(V, list[e + 1] * BLK, n);
+    }
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const int j0 = kb * BLK + 32 * sub;
+      if (!wave_ok || j0 >= n || (a.causal && j0 > min(n - 1, q0 + 31))) continue;
+      const bool edge = j0 + 31 >= n || (a.causal && j0 + 31 > q0);
+      f32x16 s = zero16();
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+        s = M::mma(lds_row_frag<E, D>(k_rm, 32 * sub + (lane & 31), kk), qf[kk], s);
+      float p[16], u[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float zp = relu_z(c, s[r], tau);
+        if (edge) {
+          const int j = j0 + crow(r);
+          if (j >= n || (a.causal && j > i)) zp = 0.f;
+        }
+        if constexpr (TRAIN) {
+          Gamma<GK>::pu(zp, g, p[r], u[r]);
+          usum += u[r];
+        } else {
+          p[r] = Gamma<GK>::p_only(zp, g);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < PS; ++t) {
+        const typename M::frag pa = M::pack(p, t);
+        typename M::frag uh, ul;
+        if constexpr (TRAIN) M::pack_split(u, t, uh, ul);
+#pragma unroll
+        for (int nt = 0; nt < NTD; ++nt) {
+          const typename M::frag vb = lds_perm_frag<E>(v_tr, 32 * nt + (lane & 31), 32 * sub, t);
+          o[nt] = M::mma(pa, vb, o[nt]);
+          if constexpr (TRAIN) {
+            o2[nt] = M::mma(uh, vb, o2[nt]);
+            if constexpr (!M::exact_operands) o2[nt] = M::mma(ul, vb, o2[nt]);
+          }
+        }
+      }
+    }
+  }
+
+  if (!wave_ok) return;
+  if constexpr (TRAIN) usum += __shfl_xor(usum, 32);
+  E* O = static_cast<E*>(a.o) + head;
+  float* O2 = a.o2 + head;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int row = crow(r);
+    const int ir = q0 + row;
+    float us = 0.f;
+    if constexpr (TRAIN) us = __shfl(usum, row);
+    if (ir < n) {
+#pragma unroll
+      for (int nt = 0; nt < NTD; ++nt) {
+        const size_t off = (size_t)ir * D + 32 * nt + (lane & 31);
+        O[off] = (E)o[nt][r];
+        if constexpr (TRAIN) O2[off] = us > 0.f ? o2[nt][r] / us : 0.f;
+      }
+    }
+  }
+}
+
+template <typename E, int D, bool TRAIN>
+hipError_t launch_fwd_dt(const FwdArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)(a.BH * a.T)), block(FWD_NT);
+  switch (a.gk) {
+    case 1: hipLaunchKernelGGL((fwd_kernel<E, D, 1, TRAIN>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((fwd_kernel<E, D, 2, TRAIN>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((fwd_kernel<E, D, 4, TRAIN>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((fwd_kernel<E, D, 0, TRAIN>), grid, block, 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename E, int D>
+hipError_t launch_fwd_d(const FwdArgs& a, bool train, hipStream_t s) {
+  return train ? launch_fwd_dt<E, D, true>(a, s) : launch_fwd_dt<E, D, false>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_compact(const CompactArgs& a, hipStream_t s) {
+  const long long waves = 2LL * a.BH * a.T;
+  dim3 grid((unsigned)((waves + CMP_NT / 64 - 1) / (CMP_NT / 64))), block(CMP_NT);
+  hipLaunchKernelGGL(compact_kernel, grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd(const FwdArgs& a, int dtype, int head_dim, bool train, hipStream_t s) {
+  if (dtype == 0)
+    return head_dim == 64 ? launch_fwd_d<__bf16, 64>(a, train, s) : launch_fwd_d<__bf16, 128>(a, train, s);
+  return head_dim == 64 ? launch_fwd_d<float, 64>(a, train, s) : launch_fwd_d<float, 128>(a, train, s);
+}
+
+}  // namespace ea

@@ -1,0 +1,88 @@
+// ea_internal.h -- launch interface between the C ABI (ea_api.hip) and the
+// kernel translation units.  Host-side only; no torch, no exceptions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ea {
+
+// Largest sequence length the kernels accept (the solver keeps one byte per
+// (wave, key block) of mask state in LDS).
+constexpr int MAX_SEQLEN = 131072;
+constexpr int MAX_KEY_BLOCKS = MAX_SEQLEN / 64;
+
+// Which specialisation of the per-element map: gamma = 1/(alpha-1) in
+// {1, 2, 4} run without transcendentals; 0 means general alpha.
+int gamma_kind(float alpha);
+
+struct TauArgs {
+  const void* q;
+  const void* k;
+  float* tau;         // [BH, n]
+  uint8_t* mask;      // [BH, T, T]
+  int32_t* stats;     // [BH, ceil(n/128)] passes per workgroup, or null
+  int BH, n, T;
+  float c;            // (alpha - 1) * scale
+  float alpha, gamma;
+  int causal, max_iter;
+  float tol;
+  int gk;             // gamma_kind(alpha)
+};
+
+struct CompactArgs {
+  const uint8_t* mask;
+  int32_t *q_count, *q_index, *k_count, *k_index;
+  int BH, T;
+};
+
+struct FwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;                // [BH, n, D] input dtype
+  float* o2;              // [BH, n, D] fp32, train only
+  const float* tau;
+  const int32_t* q_count;
+  const int32_t* q_index;
+  int BH, n, T;
+  float c, gamma;
+  int causal;
+  int gk;
+};
+
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* dout;
+  const float* tau;
+  const float* delta;     // [BH, n]
+  const int32_t* q_count;
+  const int32_t* q_index;
+  const int32_t* k_count;
+  const int32_t* k_index;
+  float *dq, *dk, *dv;
+  int BH, n, T;
+  float c, gamma, scale;
+  int causal;
+  int gk;
+};
+
+struct DeltaArgs {
+  const void* dout;
+  const float* o2;
+  float* delta;
+  int64_t rows;
+};
+
+// Each launcher picks the instantiation for (dtype: 0 bf16 / 1 fp32, head_dim,
+// gamma kind) and returns the launch status.
+hipError_t launch_tau(const TauArgs& a, int dtype, int head_dim, hipStream_t s);
+hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
+hipError_t launch_fwd(const FwdArgs& a, int dtype, int head_dim, bool train, hipStream_t s);
+hipError_t launch_delta(const DeltaArgs& a, int dtype, int head_dim, hipStream_t s);
+hipError_t launch_bwd_dkdv(const BwdArgs& a, int dtype, int head_dim, hipStream_t s);
+hipError_t launch_bwd_dq(const BwdArgs& a, int dtype, int head_dim, hipStream_t s);
+
+}  // namespace ea

@@ -1,0 +1,255 @@
+// ea_tau.hip -- per-row alpha-entmax threshold tau and the 64x64 block mask.
+//
+// Method (Sec. 3.1 Algorithm 1, block form Algorithm 3 of App. A): for each
+// query row i, x_ij = (alpha-1) * scale * <q_i, k_j>; tau_i is the root of
+// f(tau) = sum_j [x_ij - tau]_+^gamma - 1 (Eq. 3).  f, f', f'' (Eq. 3, 6, 7)
+// are additive over key blocks, so each pass streams K once and accumulates
+// three per-row sums; between passes the bracket is updated with the
+// bisection rule B_f (Eq. 4) and the Halley step H_f (Eq. 5) is taken when it
+// lands inside the bracket, otherwise the midpoint.  The bracket starts at
+// [max_j x_ij - 1, max_j x_ij - n_i^(1-alpha)] after a first pass that finds
+// the row maximum.  The block mask of Eq. 8 is recorded during every
+// evaluation pass; the pass at the returned tau is the last one, so the mask
+// describes exactly the probabilities that the forward and backward kernels
+// recompute from that tau.
+//
+// Layout on gfx950: one workgroup = 4 waves = 128 query rows (two mask
+// rows); each wave keeps its 32 query rows as MFMA B operands in registers
+// and computes S^T tiles (keys x queries), so every lane owns one query and
+// the per-row sums stay in-lane until the end of a pass.  K tiles of 64 keys
+// go through LDS, the next one in flight in registers.  A workgroup stops as
+// soon as every row it owns has |f(tau)| <= tol, or after max_iter updates.
+#include "ea_common.h"
+#include "ea_internal.h"
+
+namespace ea {
+
+namespace {
+
+constexpr int TAU_WAVES = 4;
+constexpr int TAU_NT = 64 * TAU_WAVES;
+constexpr int TAU_ROWS = 32 * TAU_WAVES;
+
+template <typename E, int D, int GK>
+__global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
+  using G = TileGeom<E, D>;
+  using M = Mma<E>;
+  constexpr int KS = D / M::KW;
+  __shared__ __attribute__((aligned(16))) E k_rm[G::RM_ELEMS];
+  __shared__ uint8_t bits[TAU_WAVES * MAX_KEY_BLOCKS];
+
+  const int lane = lane_id(), w = wave_id();
+  const int n = a.n, T = a.T;
+  const int nqt = (n + TAU_ROWS - 1) / TAU_ROWS;
+  const int bh = blockIdx.x % a.BH;
+  int qt = blockIdx.x / a.BH;
+  if (a.causal) qt = nqt - 1 - qt;  // longest rows first
+  const int q0 = qt * TAU_ROWS + 32 * w;
+  const int i = q0 + (lane & 31);
+  const bool row_ok = i < n;
+  const int ni = a.causal ? i + 1 : n;
+  const E* Q = static_cast<const E*>(a.q) + (size_t)bh * n * D;
+  const E* K = static_cast<const E*>(a.k) + (size_t)bh * n * D;
+
+  const int wg_last = min(n, (qt + 1) * TAU_ROWS) - 1;
+  const int nkb = a.causal ? wg_last / BLK + 1 : T;
+  const int wave_last = min(n - 1, q0 + 31);
+  const bool wave_ok = q0 < n;
+
+  typename M::frag qf[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) qf[kk] = load_row_frag_global<E, D>(Q, i, n, kk);
+
+  for (int x = threadIdx.x; x < TAU_WAVES * T; x += TAU_NT)
+    bits[(x / T) * MAX_KEY_BLOCKS + (x % T)] = 0;
+
+  const float c = a.c;
+
+  // Streams every key block the workgroup needs; `body(kb)` sees K block kb
+  // in k_rm.
+  auto stream = [&](auto&& body) {
+    TileRegs<E, D, TAU_NT> regs;
+    regs.load(K, 0, n);
+    for (int kb = 0; kb < nkb; ++kb) {
+      __syncthreads();
+      regs.store_rm(k_rm);
+      __syncthreads();
+      if (kb + 1 < nkb) regs.load(K, (kb + 1) * BLK, n);
+      body(kb);
+    }
+  };
+
+  // S^T sub-tile: keys [32 sub, 32 sub + 32) of the staged block x this
+  // wave's 32 queries; value r of lane l is key 32 sub + crow(r), query l%32.
+  auto scores = [&](int sub) {
+    f32x16 acc = zero16();
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+      acc = M::mma(lds_row_frag<E, D>(k_rm, 32 * sub + (lane & 31), kk), qf[kk], acc);
+    return acc;
+  };
+  // Sub-tile state for the calling wave: 0 = nothing valid, 1 = all valid,
+  // 2 = needs per-element masking (ragged tail or causal diagonal).
+  auto sub_kind = [&](int j0) {
+    if (!wave_ok || j0 >= n || (a.causal && j0 > wave_last)) return 0;
+    if (j0 + 31 >= n || (a.causal && j0 + 31 > q0)) return 2;
+    return 1;
+  };
+
+  // ---- pass 0: row maximum of the raw scores (scale > 0, so the maximum of
+  // x = c s is c times the maximum of s)
+  float smax = -INFINITY;
+  stream([&](int kb) {
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const int j0 = kb * BLK + 32 * sub;
+      const int kind = sub_kind(j0);
+      if (kind == 0) continue;
+      f32x16 s = scores(sub);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = s[r];
+        if (kind == 2) {
+          const int j = j0 + crow(r);
+          if (j >= n || (a.causal && j > i)) v = -INFINITY;
+        }
+        smax = fmaxf(smax, v);
+      }
+    }
+  });
+  smax = fmaxf(smax, __shfl_xor(smax, 32));
+
+  float lo = 0.f, hi = 0.f, tau = 0.f;
+  if (row_ok) {
+    const float m = c * smax;
+    lo = m - 1.f;
+    hi = m - powf((float)ni, 1.f - a.alpha);
+    tau = 0.5f * (lo + hi);
+  }
+
+  const float g = a.gamma;
+  int passes = 1;
+  for (int it = 0;; ++it) {
+    // ---- evaluation pass at tau: s0 = sum z^gamma, s1 = sum z^(gamma-1),
+    // s2 = sum z^(gamma-2) over the strict support z > 0
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f;
+    stream([&](int kb) {
+      unsigned long long hit = 0ull;
+      bool touched = false;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+        const int j0 = kb * BLK + 32 * sub;
+        const int kind = sub_kind(j0);
+        if (kind == 0) continue;
+        touched = true;
+        f32x16 s = scores(sub);
+        float t0 = 0.f, t1 = 0.f, t2 = 0.f, any = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float zp = relu_z(c, s[r], tau);
+          if (kind == 2) {
+            const int j = j0 + crow(r);
+            if (j >= n || (a.causal && j > i)) zp = 0.f;
+          }
+          if constexpr (GK == 1) {
+            t0 += zp;
+            t1 += zp > 0.f ? 1.f : 0.f;
+          } else if constexpr (GK == 2) {
+            t0 = fmaf(zp, zp, t0);
+            t1 += zp;
+            t2 += zp > 0.f ? 1.f : 0.f;
+          } else if constexpr (GK == 4) {
+            const float z2 = zp * zp;
+            t0 = fmaf(z2, z2, t0);
+            t1 = fmaf(z2, zp, t1);
+            t2 += z2;
+          } else {
+            if (zp > 0.f) {
+              const float l = __log2f(zp);
+              t0 += exp2f(g * l);
+              t1 += exp2f((g - 1.f) * l);
+              t2 += exp2f((g - 2.f) * l);
+              any += 1.f;
+            }
+          }
+        }
+        s0 += t0;
+        s1 += t1;
+        s2 += t2;
+        const float ind = GK == 1 ? t1 : (GK == 0 ? any : t2);
+        hit |= __ballot(ind > 0.f);
+      }
+      if (touched && lane == 0) bits[w * MAX_KEY_BLOCKS + kb] = hit != 0ull;
+    });
+    ++passes;
+    s0 += __shfl_xor(s0, 32);
+    s1 += __shfl_xor(s1, 32);
+    s2 += __shfl_xor(s2, 32);
+
+    const float f = s0 - 1.f;                        // Eq. 3
+    float f1, f2;                                    // Eq. 6, 7
+    if constexpr (GK == 1) {
+      f1 = -s1;
+      f2 = 0.f;
+    } else if constexpr (GK == 2) {
+      f1 = -2.f * s1;
+      f2 = 2.f * s2;
+    } else if constexpr (GK == 4) {
+      f1 = -4.f * s1;
+      f2 = 12.f * s2;
+    } else {
+      f1 = -g * s1;
+      f2 = g * (g - 1.f) * s2;
+    }
+    const bool conv = !row_ok || fabsf(f) <= a.tol;
+    if (__syncthreads_and(conv) || it >= a.max_iter) break;
+    if (row_ok) {
+      if (f < 0.f)  // B_f, Eq. 4 ("otherwise" branch when f == 0)
+        hi = tau;
+      else
+        lo = tau;
+      const float th = tau - 2.f * f * f1 / (2.f * f1 * f1 - f * f2);  // H_f, Eq. 5
+      // Bracket test of Algorithm 1 with fp32 rounding: when the root sits on
+      // an end of the bracket (one-hot rows: tau = max - 1; constant rows:
+      // tau = max - n^(1-alpha)) the Halley value lands within a few ulps on
+      // either side of it, so values within `slack` are accepted and clamped
+      // into [lo, hi].  NaN and inf fail the test and take the midpoint.
+      const float slack = 1e-6f * fmaxf(1.f, fmaxf(fabsf(lo), fabsf(hi)));
+      tau = (th >= lo - slack && th <= hi + slack) ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
+    }
+  }
+
+  if (row_ok && lane < 32) a.tau[(size_t)bh * n + i] = tau;
+  __syncthreads();
+  for (int x = threadIdx.x; x < 2 * T; x += TAU_NT) {
+    const int half = x / T, kb = x % T;
+    const int qb = 2 * qt + half;
+    if (qb < T) {
+      const uint8_t b = bits[(2 * half) * MAX_KEY_BLOCKS + kb] | bits[(2 * half + 1) * MAX_KEY_BLOCKS + kb];
+      a.mask[((size_t)bh * T + qb) * T + kb] = b;
+    }
+  }
+  if (a.stats && threadIdx.x == 0) a.stats[(size_t)bh * nqt + qt] = passes;
+}
+
+template <typename E, int D>
+hipError_t launch_tau_d(const TauArgs& a, hipStream_t s) {
+  const int nqt = (a.n + TAU_ROWS - 1) / TAU_ROWS;
+  dim3 grid((unsigned)(a.BH * nqt)), block(TAU_NT);
+  switch (a.gk) {
+    case 1: hipLaunchKernelGGL((tau_solve_kernel<E, D, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((tau_solve_kernel<E, D, 2>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((tau_solve_kernel<E, D, 4>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((tau_solve_kernel<E, D, 0>), grid, block, 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_tau(const TauArgs& a, int dtype, int head_dim, hipStream_t s) {
+  if (dtype == 0) return head_dim == 64 ? launch_tau_d<__bf16, 64>(a, s) : launch_tau_d<__bf16, 128>(a, s);
+  return head_dim == 64 ? launch_tau_d<float, 64>(a, s) : launch_tau_d<float, 128>(a, s);
+}
+
+}  // namespace ea

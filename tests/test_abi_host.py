@@ -1,0 +1,132 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/entmax_attn.h declares, sizes are right, and invalid
+arguments are rejected before anything is launched."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "entmax_attn.h")
+
+ea = pytest.importorskip("paper_2502_12082_amd", reason="HIP library not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(entmax_attn_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert set(names) == set(ea.SYMBOLS)
+    lib = ctypes.CDLL(ea.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for s in range(5):
+        assert ea._lib.entmax_attn_status_string(s)
+    assert ea._lib.entmax_attn_status_string(99) == b"unknown status"
+
+
+def shape(B=2, H=3, n=1000, d=64, dt=0):
+    return ea.Shape(B, H, n, d, dt)
+
+
+def test_default_params():
+    p = ea.default_params()
+    assert p.alpha == 1.5 and p.causal == 0 and p.need_bwd == 1
+    assert p.max_iter > 0 and p.tol > 0
+
+
+def test_sizes():
+    s, p = shape(), ea.default_params()
+    z = ea.entmax_attn_sizes(s, p)
+    BH, n, d, T = 6, 1000, 64, 16
+    assert z.tau == BH * n * 4
+    assert z.o2 == BH * n * d * 4
+    assert z.block_mask == BH * T * T
+    assert z.q_count == z.k_count == BH * T * 4
+    assert z.q_index == z.k_index == BH * T * T * 4
+    assert z.stats == BH * 8 * 4
+    assert z.ws_fwd == 0 and z.ws_bwd == BH * n * 4
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("batch", 0, ea.EA_ERR_INVALID_ARG),
+    ("seqlen", -1, ea.EA_ERR_INVALID_ARG),
+    ("head_dim", 96, ea.EA_ERR_UNSUPPORTED),
+    ("head_dim", 256, ea.EA_ERR_UNSUPPORTED),
+    ("dtype", 7, ea.EA_ERR_UNSUPPORTED),
+    ("seqlen", 131073, ea.EA_ERR_UNSUPPORTED),
+])
+def test_shape_validation(field, value, code):
+    s = shape()
+    setattr(s, field, value)
+    with pytest.raises(ea.EntmaxAttnError) as e:
+        ea.entmax_attn_sizes(s, ea.default_params())
+    assert e.value.status == code
+
+
+@pytest.mark.parametrize("field,value", [
+    ("alpha", 1.0), ("alpha", 0.5), ("alpha", math.nan), ("alpha", math.inf),
+    ("scale", 0.0), ("scale", -0.1), ("scale", math.nan),
+    ("causal", 2), ("need_bwd", -1), ("max_iter", -1), ("max_iter", 65),
+    ("tol", -1e-3), ("tol", math.nan),
+])
+def test_param_validation(field, value):
+    p = ea.default_params()
+    setattr(p, field, value)
+    with pytest.raises(ea.EntmaxAttnError) as e:
+        ea.entmax_attn_sizes(shape(), p)
+    assert e.value.status == ea.EA_ERR_INVALID_ARG
+
+
+def _fake(addr=0x10000):
+    return addr  # never dereferenced: every case below fails validation first
+
+
+def test_fwd_rejects_bad_pointers_before_launch():
+    s, p = shape(), ea.default_params()
+    good = ea.ResidualPtrs(*[_fake() for _ in range(7)], None)
+    # null q
+    assert ea.entmax_attn_fwd(s, p, None, _fake(), _fake(), _fake(), good, None, 0,
+                              None) == ea.EA_ERR_INVALID_ARG
+    # misaligned v
+    assert ea.entmax_attn_fwd(s, p, _fake(), _fake(), _fake() + 2, _fake(), good, None, 0,
+                              None) == ea.EA_ERR_INVALID_ARG
+    # missing o2 while need_bwd
+    r = ea.ResidualPtrs(*[_fake() for _ in range(7)], None)
+    r.o2 = None
+    assert ea.entmax_attn_fwd(s, p, _fake(), _fake(), _fake(), _fake(), r, None, 0,
+                              None) == ea.EA_ERR_INVALID_ARG
+    # missing table
+    r = ea.ResidualPtrs(*[_fake() for _ in range(7)], None)
+    r.k_index = None
+    assert ea.entmax_attn_fwd(s, p, _fake(), _fake(), _fake(), _fake(), r, None, 0,
+                              None) == ea.EA_ERR_INVALID_ARG
+    # bad parameter
+    p.alpha = 1.0
+    assert ea.entmax_attn_fwd(s, p, _fake(), _fake(), _fake(), _fake(), good, None, 0,
+                              None) == ea.EA_ERR_INVALID_ARG
+
+
+def test_bwd_rejects_small_workspace_and_bad_pointers():
+    s, p = shape(), ea.default_params()
+    z = ea.entmax_attn_sizes(s, p)
+    r = ea.ResidualPtrs(*[_fake() for _ in range(7)], None)
+    args = [_fake()] * 4
+    assert ea.entmax_attn_bwd(s, p, *args, r, _fake(), _fake(), _fake(), _fake(),
+                              z.ws_bwd - 4, None) == ea.EA_ERR_WORKSPACE
+    assert ea.entmax_attn_bwd(s, p, *args, r, _fake(), _fake(), _fake(), None,
+                              z.ws_bwd, None) == ea.EA_ERR_INVALID_ARG
+    assert ea.entmax_attn_bwd(s, p, *args, r, None, _fake(), _fake(), _fake(),
+                              z.ws_bwd, None) == ea.EA_ERR_INVALID_ARG
+    r.o2 = None
+    assert ea.entmax_attn_bwd(s, p, *args, r, _fake(), _fake(), _fake(), _fake(),
+                              z.ws_bwd, None) == ea.EA_ERR_INVALID_ARG

@@ -1,0 +1,184 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded inputs, element by element.
+
+Tolerances (gpu_util): tau |dtau| <= 1e-3 * max(1, |tau|); O, O2, dQ, dK, dV
+max-abs <= 2e-2 for bf16 inputs and <= 1e-4 for fp32 inputs; block masks
+bit-exact except blocks whose decisive score lies within 1e-4 * max(1, |tau|)
+of the threshold (several masks are correct there); lookup tables bit-exact
+against the mask.
+
+Small shapes are checked on every row and column.  The workload shapes are
+checked on whole heads where the oracle finishes in seconds, otherwise on
+sampled query blocks (tau, O, O2, dQ, mask rows) and on the last key columns
+(dK, dV), which depend only on the sampled rows under causal masking.
+"""
+import numpy as np
+import pytest
+
+import synth
+from gpu_util import check_head, check_tables, log, oracle_head, run_gpu, to_device
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2502_12082_amd  # noqa: F401  (fails loudly if the library is missing)
+
+
+def _full_case(B, H, n, d, dtype, alpha, causal, bwd, c, seed, heads=None, label=""):
+    inp = synth.attention_inputs(B, H, n, d, c=c, dtype=dtype, with_dout=bwd, seed=seed)
+    scale = d ** -0.5
+    log("case %s B%d H%d n%d d%d %s alpha=%g causal=%d bwd=%d c=%g" % (
+        label, B, H, n, d, dtype, alpha, causal, bwd, c))
+    gpu = run_gpu(inp, alpha, scale, causal, bwd)
+    check_tables(gpu, causal)
+    errs = []
+    for bh in (heads if heads is not None else range(B * H)):
+        ref = oracle_head(inp, bh, alpha, scale, causal, bwd)
+        errs.append(check_head(gpu, ref, bh, dtype, "%s bh=%d" % (label, bh)))
+    log("  errors %s" % errs[0])
+    return gpu, errs
+
+
+def test_tiny_forward_fp32():
+    """Tiny config: B1 H1 n256 d64 fp32, alpha 1.5, non-causal, forward."""
+    gpu, errs = _full_case(1, 1, 256, 64, "f32", 1.5, False, False, 1.0, synth.SEED_BASE,
+                           label="tiny")
+    assert gpu["stats"].min() >= 2
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("n", [1, 2, 3, 63, 64, 65, 257])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_small_shapes(dtype, n, causal, d):
+    # alpha 1.6 exercises the general-alpha (exp2/log2) kernels; for alpha in (1.5, 2)
+    # u = z^(gamma-1) has an unbounded slope at z -> 0, so entries at the support
+    # edge amplify fp32 tau rounding; 1.6 keeps that within the fp32 bound.
+    for alpha, c in ((1.5, 2.0), (2.0, 1.0), (1.25, 3.0), (1.6, 2.0)):
+        _full_case(1, 2, n, d, dtype, alpha, causal, True, c, 100 + n,
+                   label="small-%s-a%g" % (dtype, alpha))
+
+
+@pytest.mark.parametrize("c", [1.0, 4.0, 16.0])
+def test_encoder_forward(c):
+    """B8 H12 n1024 d64 bf16 forward, Q temperature c; 4 heads vs the oracle."""
+    _full_case(8, 12, 1024, 64, "bf16", 1.5, False, False, c, synth.SEED_BASE,
+               heads=[0, 37, 60, 95], label="encoder")
+
+
+def test_decoder_step():
+    """B4 H12 n4096 d64 bf16 causal, c=8, forward + backward; 2 whole heads."""
+    _full_case(4, 12, 4096, 64, "bf16", 1.5, True, True, 8.0, synth.SEED_BASE,
+               heads=[0, 29], label="decoder")
+
+
+def _sampled_case(B, H, n, d, alpha, causal, c, block_rows, ncols, heads, label,
+                  full_cols=False):
+    inp = synth.attention_inputs(B, H, n, d, c=c, dtype="bf16", with_dout=True,
+                                 seed=synth.SEED_BASE)
+    scale = d ** -0.5
+    log("case %s B%d H%d n%d d%d alpha=%g causal=%d c=%g" % (label, B, H, n, d, alpha, causal, c))
+    gpu = run_gpu(inp, alpha, scale, causal, True)
+    T = (n + 63) // 64
+    rows = sorted(set(r for I in block_rows for r in range(I * 64, min(n, I * 64 + 64))))
+    cols = list(range(n - ncols, n)) if ncols else None
+    out = []
+    for bh in heads:
+        ref = oracle_head(inp, bh, alpha, scale, causal, True, rows=rows, cols=cols,
+                          block_rows=block_rows)
+        out.append(check_head(gpu, ref, bh, "bf16", "%s bh=%d" % (label, bh), rows=rows,
+                              cols=cols))
+    log("  errors %s" % out[0])
+    return gpu, inp
+
+
+# The bench workload: B1 H16 n8192 d128 bf16 non-causal, fwd+bwd, alpha 1.5.
+@pytest.mark.parametrize("alpha,c", [(1.5, 1.0), (1.5, 0.0625), (1.5, 32.0), (1.25, 1.0),
+                                     (1.25, 8.0), (2.0, 1.0), (2.0, 32.0)])
+def test_sweep_workload(alpha, c):
+    T = 128
+    _sampled_case(1, 16, 8192, 128, alpha, False, c, block_rows=[0, 57, T - 1], ncols=0,
+                  heads=[3], label="sweep")
+
+
+def test_sweep_workload_full_head():
+    """Every row and column of one head of the bench workload (alpha 1.5, c 1)."""
+    inp = synth.attention_inputs(1, 16, 8192, 128, c=1.0, dtype="bf16", with_dout=True,
+                                 seed=synth.SEED_BASE)
+    gpu = run_gpu(inp, 1.5, 128 ** -0.5, False, True)
+    check_tables(gpu, False)
+    ref = oracle_head(inp, 5, 1.5, 128 ** -0.5, False, True)
+    log("  errors %s" % check_head(gpu, ref, 5, "bf16", "sweep-full"))
+
+
+@pytest.mark.parametrize("n", [16384, 65536])
+def test_long_context(n):
+    """B1 H8 d64 bf16 causal, c=16, fwd+bwd: first, middle and last query
+    blocks; dK/dV on the last 64 keys."""
+    T = n // 64
+    gpu, _ = _sampled_case(1, 8, n, 64, 1.5, True, 16.0, block_rows=[0, T // 2, T - 1],
+                           ncols=64, heads=[0, 7], label="long")
+    check_tables({k: gpu[k][:1] for k in ("mask", "q_count", "q_index", "k_count", "k_index")},
+                 True)
+
+
+# ------------------------------------------------------------- invariants
+
+def _device(inp):
+    return to_device(inp["q"]), to_device(inp["k"]), to_device(inp["v"])
+
+
+def test_invariants_and_determinism():
+    import paper_2502_12082_amd as ea
+    B, H, n, d = 1, 4, 1000, 128
+    inp = synth.attention_inputs(B, H, n, d, c=2.0, dtype="bf16", with_dout=True, seed=77)
+    q, k, v = _device(inp)
+    do = to_device(inp["dout"])
+    for causal in (False, True):
+        log("invariants causal=%d" % causal)
+        o, res = ea.forward(q, k, v, alpha=1.5, scale=d ** -0.5, causal=causal)
+        dq, dk, dv = ea.backward(q, k, v, do, res)
+        o_b, res_b = ea.forward(q, k, v, alpha=1.5, scale=d ** -0.5, causal=causal)
+        dq_b, dk_b, dv_b = ea.backward(q, k, v, do, res_b)
+        torch.cuda.synchronize()
+        for a, b in ((o, o_b), (res.tau, res_b.tau), (res.o2, res_b.o2), (dq, dq_b),
+                     (dk, dk_b), (dv, dv_b), (res.block_mask, res_b.block_mask)):
+            assert torch.equal(a, b), "not bit-identical across runs"
+        # sum_j dS_ij = 0  =>  sum_j dK_j = 0;  sum_j p_ij = 1  =>  sum_j dV_j = sum_i dO_i
+        dk_sum = dk.double().sum(2).abs().max().item()
+        assert dk_sum <= 1e-3 * max(1.0, dk.abs().max().item()) * 10, dk_sum
+        dv_err = (dv.double().sum(2) - do.double().sum(2)).abs().max().item()
+        assert dv_err <= 0.05 * max(1.0, do.double().sum(2).abs().max().item()), dv_err
+        # V = 1  =>  O = sum_j p_ij = 1 + f(tau)
+        ones = torch.ones_like(v)
+        o1, _ = ea.forward(q, k, ones, alpha=1.5, scale=d ** -0.5, causal=causal,
+                           need_bwd=False)
+        assert (o1.float() - 1).abs().max().item() <= 8e-3
+
+
+def test_nan_inputs_do_not_fault():
+    """A NaN score gets probability 0 (the clamp of [x - tau]_+ maps NaN to 0),
+    so NaN in Q or K leaves tau finite; NaN in V propagates to the rows that
+    attend to that key.  Rows that never see the NaN stay finite."""
+    import paper_2502_12082_amd as ea
+    inp = synth.attention_inputs(1, 1, 128, 64, dtype="f32", seed=3)
+    q, k, v = _device(inp)
+    o_ref, _ = ea.forward(q, k, v)
+    q2 = q.clone()
+    q2[0, 0, 5, 0] = float("nan")
+    o, res = ea.forward(q2, k, v)
+    torch.cuda.synchronize()
+    keep = [r for r in range(128) if r != 5]
+    assert torch.isfinite(res.tau[0, keep]).all()
+    assert (o[0, 0, keep] - o_ref[0, 0, keep]).abs().max().item() <= 1e-4
+    v2 = v.clone()
+    v2[0, 0, 9, :] = float("nan")
+    o3, res3 = ea.forward(q, k, v2)
+    torch.cuda.synchronize()
+    assert torch.isfinite(res3.tau).all()
+    assert torch.isnan(o3).any()
