@@ -1,0 +1,269 @@
+"""Benchmark: alpha-entmax flash attention forward + backward on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+
+Workload (the sparsity-sweep shape): batch 1, 16 heads, n = 8192, d = 128,
+bf16 inputs, non-causal, alpha = 1.5, scale = 1/sqrt(d); Q ~ c N(0,1),
+K, V, dO ~ N(0,1), seeded synthetic data.  One step = the whole path: tau
+solver, table compaction, sparse forward (with O2), delta, dK/dV, dQ, each
+launched through the C ABI stage entry points on the current stream.
+
+Prints ONE JSON line.  `value` is dense-equivalent TFLOP/s (14 n^2 d per head
+for forward + backward, the FlashAttention convention) at the headline
+temperature c; `executed_tflops` counts the MFMA work the method actually
+performs (solver passes over every valid block, 10 block products per listed
+block).  `roofline` is for the kernel with the largest share of the step,
+timed with HIP events over the timed region; `cpu_baseline` is the fp64
+oracle on a bounded sample (one head), on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "fwd+bwd ms & effective TFLOP/s vs sparsity, n=8192 d=128 α=1.5 (1 GPU)"
+PEAK_BF16_TFLOPS = 2500.0
+KERNELS = ("tau_solve", "compact", "fwd_sparse", "bwd_delta", "bwd_dkdv", "bwd_dq")
+# MFMA block products (64 x 64 x d each) per listed block, by kernel
+PRODUCTS_PER_ACTIVE = {"fwd_sparse": 3, "bwd_dkdv": 4, "bwd_dq": 3}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--c", type=float, default=1.0, help="headline query temperature")
+    ap.add_argument("--sweep", type=str, default="0.0625,0.25,1,4,16,32",
+                    help="extra temperatures reported in 'sweep' (empty: none)")
+    ap.add_argument("--sweep-steps", type=int, default=5)
+    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--heads", type=int, default=16)
+    ap.add_argument("--seqlen", type=int, default=8192)
+    ap.add_argument("--head-dim", type=int, default=128)
+    ap.add_argument("--alpha", type=float, default=1.5)
+    ap.add_argument("--causal", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=4, help="heads in the oracle sample")
+    return ap.parse_args()
+
+
+class Runner:
+    """Device buffers and the six stage launches of one configuration."""
+
+    def __init__(self, args, c):
+        import torch
+        import synth
+        import paper_2502_12082_amd as ea
+        self.ea, self.torch = ea, torch
+        B, H, n, d = args.batch, args.heads, args.seqlen, args.head_dim
+        self.B, self.H, self.n, self.d, self.c = B, H, n, d, c
+        inp = synth.attention_inputs(B, H, n, d, c=c, dtype="bf16", with_dout=True)
+        self.inp = inp
+        dev = lambda t: torch.from_numpy(t.raw.view(np.int16)).view(torch.bfloat16).cuda()
+        self.q, self.k, self.v, self.do = (dev(inp[x]) for x in ("q", "k", "v", "dout"))
+        self.shape = ea.make_shape(self.q)
+        self.params = ea.make_params(args.alpha, d ** -0.5, args.causal, True, head_dim=d)
+        self.res = ea.Residuals(self.shape, self.params, self.q.device)
+        self.rp = self.res.ptrs()
+        self.o = torch.empty_like(self.q)
+        f32 = lambda: torch.empty(self.q.shape, dtype=torch.float32, device=self.q.device)
+        self.dq, self.dk, self.dv = f32(), f32(), f32()
+        self.ws = torch.empty(self.res.sizes.ws_bwd // 4 + 4, dtype=torch.float32,
+                              device=self.q.device)
+        self.events = [[torch.cuda.Event(enable_timing=True) for _ in range(7)]
+                       for _ in range(max(1, args.steps))]
+
+    def step(self, ev=None):
+        ea, s = self.ea, self.torch.cuda.current_stream().cuda_stream
+        q, k, v, do = self.q.data_ptr(), self.k.data_ptr(), self.v.data_ptr(), self.do.data_ptr()
+        if ev:
+            ev[0].record()
+        for st in range(3):
+            ea._check(ea.entmax_attn_fwd_stage(st, self.shape, self.params, q, k, v,
+                                               self.o.data_ptr(), self.rp, s), "fwd stage")
+            if ev:
+                ev[1 + st].record()
+        for st in range(3):
+            ea._check(ea.entmax_attn_bwd_stage(st, self.shape, self.params, q, k, v, do, self.rp,
+                                               self.dq.data_ptr(), self.dk.data_ptr(),
+                                               self.dv.data_ptr(), self.ws.data_ptr(),
+                                               self.ws.numel() * 4, s), "bwd stage")
+            if ev:
+                ev[4 + st].record()
+
+    def timed(self, steps, warmup, per_kernel=True):
+        torch = self.torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        wall0 = time.perf_counter()
+        t_start.record()
+        for i in range(steps):
+            self.step(self.events[i] if per_kernel else None)
+        t_end.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        total_ms = t_start.elapsed_time(t_end)
+        kern = None
+        if per_kernel:
+            kern = {name: 0.0 for name in KERNELS}
+            for i in range(steps):
+                ev = self.events[i]
+                for j, name in enumerate(KERNELS):
+                    kern[name] += ev[j].elapsed_time(ev[j + 1])
+            kern = {k_: v_ / steps for k_, v_ in kern.items()}
+        return total_ms / steps, wall, kern
+
+    def work(self):
+        """Block counts and FLOPs of the last step (from its mask and stats)."""
+        n, d, BH = self.n, self.d, self.B * self.H
+        T = (n + 63) // 64
+        f_blk = 2.0 * 64 * 64 * d
+        mask = self.res.block_mask.cpu().numpy()
+        if self.params.causal:
+            n_valid = BH * T * (T + 1) // 2
+        else:
+            n_valid = BH * T * T
+        n_act = int(self.res.q_count.sum().item())
+        stats = self.res.stats.cpu().numpy().astype(np.int64)
+        nqt = (n + 127) // 128
+        # valid 64x64 blocks each 128-row solver workgroup streams
+        per_wg = np.empty(nqt, dtype=np.int64)
+        for qt in range(nqt):
+            rows = min(2, T - 2 * qt)
+            if self.params.causal:
+                per_wg[qt] = sum(min(T, 2 * qt + r + 1) for r in range(rows))
+            else:
+                per_wg[qt] = rows * T
+        solver_blocks = float((stats.reshape(BH, nqt) * per_wg[None, :]).sum())
+        flops = {"tau_solve": solver_blocks * f_blk, "compact": 0.0, "bwd_delta": 0.0}
+        for k_, m in PRODUCTS_PER_ACTIVE.items():
+            flops[k_] = m * n_act * f_blk
+        dense = 14.0 * n * n * d * BH * (0.5 if self.params.causal else 1.0)
+        return {"n_valid": n_valid, "n_act": n_act, "block_density": n_act / n_valid,
+                "passes_mean": float(stats.mean()), "passes_max": int(stats.max()),
+                "flops": flops, "dense_flops": dense, "mask_nnz": int(mask.sum())}
+
+    def zero_fraction(self, rows=64):
+        """Fraction of zero probabilities on sampled rows of head 0, from the
+        returned tau (host numpy; a statistic, not part of the timed path)."""
+        q = self.inp["q"].f64()[0, 0]
+        k = self.inp["k"].f64()[0, 0]
+        tau = self.res.tau[0].cpu().numpy().astype(np.float64)
+        idx = np.linspace(0, self.n - 1, rows).astype(int)
+        x = (self.params.alpha - 1) * self.params.scale * (q[idx] @ k.T) - tau[idx, None]
+        if self.params.causal:
+            x = np.where(np.arange(self.n)[None, :] <= idx[:, None], x, -1.0)
+            valid = (idx + 1).sum()
+        else:
+            valid = rows * self.n
+        return 1.0 - float((x > 0).sum()) / valid
+
+
+def cpu_baseline(runner, heads):
+    """The oracle (fp64, all host cores) on `heads` heads of the same workload:
+    tau, O, O2, block margins, delta, dQ, dK, dV of every row and column."""
+    import oracle
+    inp = runner.inp
+    heads = max(1, min(heads, runner.B * runner.H))
+    oracle.build()
+    sec = 0.0
+    for bh in range(heads):
+        b, h = divmod(bh, runner.H)
+        q, k, v, do = (inp[x].f64()[b, h] for x in ("q", "k", "v", "dout"))
+        t0 = time.perf_counter()
+        oracle.attention_head(q, k, v, runner.params.alpha, runner.params.scale,
+                              bool(runner.params.causal), dout=do)
+        sec += time.perf_counter() - t0
+    flops = heads * 14.0 * runner.n * runner.n * runner.d * (0.5 if runner.params.causal else 1.0)
+    return {"value": flops / sec / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": "%d of %d heads (all %d rows and columns), fwd+bwd, %.1f s; dense-equivalent "
+                      "FLOPs of the sample / time" % (heads, runner.B * runner.H, runner.n, sec)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the alpha-entmax path here is a single-GPU "
+              "build (heads would shard across GPUs with no communication); --gpus %d is not "
+              "supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    steps = max(1, args.steps)
+    run = Runner(args, args.c)
+    ms, wall, kern = run.timed(steps, args.warmup)
+    work = run.work()
+    dense_tflops = work["dense_flops"] / (ms * 1e-3) / 1e12
+    executed = sum(work["flops"].values())
+    kernels = {}
+    for name in KERNELS:
+        t = kern[name]
+        kernels[name] = {"ms": round(t, 4),
+                         "tflops": round(work["flops"][name] / (t * 1e-3) / 1e12, 2) if t > 0 else 0.0}
+    dom = max(("tau_solve", "fwd_sparse", "bwd_dkdv", "bwd_dq"), key=lambda k_: kern[k_])
+    ach = work["flops"][dom] / (kern[dom] * 1e-3) / 1e12
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                "traffic": None}
+    out = {
+        "metric": METRIC, "value": round(dense_tflops, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian Q*c, K, V, dO)",
+        "config": {"workload": "alpha-entmax attention fwd+bwd, B%d H%d n%d d%d bf16 %s, "
+                               "alpha %g, c %g" % (args.batch, args.heads, args.seqlen,
+                                                   args.head_dim,
+                                                   "causal" if args.causal else "non-causal",
+                                                   args.alpha, args.c),
+                   "batch": args.batch, "heads": args.heads, "seqlen": args.seqlen,
+                   "head_dim": args.head_dim, "alpha": args.alpha, "c": args.c,
+                   "causal": bool(args.causal)},
+        "executed_tflops": round(executed / (ms * 1e-3) / 1e12, 3),
+        "executed_frac_of_peak": round(executed / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "wall_s_timed": round(wall, 4),
+        "kernels": kernels,
+        "sparsity": {"block_density": round(work["block_density"], 4),
+                     "zero_fraction_sampled": round(run.zero_fraction(), 5),
+                     "solver_passes_mean": round(work["passes_mean"], 3),
+                     "solver_passes_max": work["passes_max"]},
+        "roofline": roofline,
+    }
+    sweep = []
+    for cs in [s for s in args.sweep.split(",") if s.strip()]:
+        cval = float(cs)
+        r = Runner(args, cval)
+        msv, _, _ = r.timed(max(1, args.sweep_steps), 2, per_kernel=False)
+        w = r.work()
+        sweep.append({"c": cval, "ms": round(msv, 4),
+                      "tflops_dense_equiv": round(w["dense_flops"] / (msv * 1e-3) / 1e12, 3),
+                      "tflops_executed": round(sum(w["flops"].values()) / (msv * 1e-3) / 1e12, 3),
+                      "block_density": round(w["block_density"], 4),
+                      "zero_fraction_sampled": round(r.zero_fraction(), 5),
+                      "solver_passes_mean": round(w["passes_mean"], 3)})
+        del r
+        torch.cuda.empty_cache()
+    if sweep:
+        out["sweep"] = sweep
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(run, args.cpu_heads)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

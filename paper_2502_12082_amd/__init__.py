@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libentmax_attn.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError("libentmax_attn.so is not built; run `python -m paper_2502_12082_amd.build` "
+    raise ImportError("libentmax_attn.so is not built; run `python paper_2502_12082_amd/build.py` "
                       "(or __graft_entry__.build()) first")
 
 _lib = ctypes.CDLL(LIB_PATH)
@@ -26,7 +26,8 @@ _lib = ctypes.CDLL(LIB_PATH)
 EA_OK, EA_ERR_INVALID_ARG, EA_ERR_UNSUPPORTED, EA_ERR_WORKSPACE, EA_ERR_HIP = range(5)
 EA_BF16, EA_F32 = 0, 1
 SYMBOLS = ("entmax_attn_default_params", "entmax_attn_sizes", "entmax_attn_fwd",
-           "entmax_attn_bwd", "entmax_attn_status_string")
+           "entmax_attn_bwd", "entmax_attn_fwd_stage", "entmax_attn_bwd_stage",
+           "entmax_attn_status_string")
 
 
 class Shape(ctypes.Structure):
@@ -64,6 +65,12 @@ _lib.entmax_attn_fwd.restype = ctypes.c_int
 _lib.entmax_attn_bwd.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _P(ResidualPtrs), _v, _v,
                                  _v, _v, ctypes.c_size_t, _v]
 _lib.entmax_attn_bwd.restype = ctypes.c_int
+_lib.entmax_attn_fwd_stage.argtypes = [ctypes.c_int, _P(Shape), _P(Params), _v, _v, _v, _v,
+                                       _P(ResidualPtrs), _v]
+_lib.entmax_attn_fwd_stage.restype = ctypes.c_int
+_lib.entmax_attn_bwd_stage.argtypes = [ctypes.c_int, _P(Shape), _P(Params), _v, _v, _v, _v,
+                                       _P(ResidualPtrs), _v, _v, _v, _v, ctypes.c_size_t, _v]
+_lib.entmax_attn_bwd_stage.restype = ctypes.c_int
 _lib.entmax_attn_status_string.argtypes = [ctypes.c_int]
 _lib.entmax_attn_status_string.restype = ctypes.c_char_p
 
@@ -105,6 +112,18 @@ def entmax_attn_bwd(shape, params, q, k, v, dout, res: ResidualPtrs, dq, dk, dv,
                     ws_bytes, stream):
     return _lib.entmax_attn_bwd(ctypes.byref(shape), ctypes.byref(params), q, k, v, dout,
                                 ctypes.byref(res), dq, dk, dv, workspace, ws_bytes, stream)
+
+
+def entmax_attn_fwd_stage(stage, shape, params, q, k, v, o, res: ResidualPtrs, stream):
+    return _lib.entmax_attn_fwd_stage(stage, ctypes.byref(shape), ctypes.byref(params), q, k, v,
+                                      o, ctypes.byref(res), stream)
+
+
+def entmax_attn_bwd_stage(stage, shape, params, q, k, v, dout, res: ResidualPtrs, dq, dk, dv,
+                          workspace, ws_bytes, stream):
+    return _lib.entmax_attn_bwd_stage(stage, ctypes.byref(shape), ctypes.byref(params), q, k, v,
+                                      dout, ctypes.byref(res), dq, dk, dv, workspace, ws_bytes,
+                                      stream)
 
 
 # ------------------------------------------------------ torch conveniences

@@ -1,6 +1,6 @@
 """Builds libentmax_attn.so (the HIP kernels plus the C ABI) for gfx950.
 
-    python -m paper_2502_12082_amd.build        # from the repository root
+    python paper_2502_12082_amd/build.py        # from the repository root
 
 Every .hip file under csrc/ is compiled with hipcc into _build/, in parallel,
 and linked into paper_2502_12082_amd/libentmax_attn.so next to this file.

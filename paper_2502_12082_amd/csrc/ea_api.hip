@@ -110,33 +110,98 @@ ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_s
   return EA_OK;
 }
 
+namespace {
+
+// Checks shared by the forward entry points; fills the kernel arguments.
+ea_status prep_fwd(const ea_shape* shape, const ea_params* params, const void* q, const void* k,
+                   const void* v, void* o, const ea_residuals* res, Dims* d) {
+  ea_status st = check_shape(shape, params, d);
+  if (st != EA_OK) return st;
+  if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(o)) return EA_ERR_INVALID_ARG;
+  if ((st = check_tables(res)) != EA_OK) return st;
+  if (params->need_bwd && !tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
+  return EA_OK;
+}
+
+ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const void* q,
+                        const void* k, const void* v, void* o, const ea_residuals* res,
+                        hipStream_t s) {
+  const float c = (params->alpha - 1.0f) * params->scale;
+  const float gamma = 1.0f / (params->alpha - 1.0f);
+  const int gk = gamma_kind(params->alpha);
+  if (stage == 0) {
+    TauArgs ta{q, k, res->tau, res->block_mask, res->stats, (int)d.BH, (int)d.n, (int)d.T,
+               c, params->alpha, gamma, params->causal, params->max_iter, params->tol, gk};
+    return from_hip(launch_tau(ta, d.dtype, (int)d.d, s));
+  }
+  if (stage == 1) {
+    CompactArgs ca{res->block_mask, res->q_count, res->q_index, res->k_count, res->k_index,
+                   (int)d.BH, (int)d.T};
+    return from_hip(launch_compact(ca, s));
+  }
+  FwdArgs fa{q, k, v, o, params->need_bwd ? res->o2 : nullptr, res->tau, res->q_count,
+             res->q_index, (int)d.BH, (int)d.n, (int)d.T, c, gamma, params->causal, gk};
+  return from_hip(launch_fwd(fa, d.dtype, (int)d.d, params->need_bwd != 0, s));
+}
+
+ea_status prep_bwd(const ea_shape* shape, const ea_params* params, const void* q, const void* k,
+                   const void* v, const void* dout, const ea_residuals* res, const float* dq,
+                   const float* dk, const float* dv, const void* workspace, size_t ws_bytes,
+                   Dims* d) {
+  ea_status st = check_shape(shape, params, d);
+  if (st != EA_OK) return st;
+  if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(dout)) return EA_ERR_INVALID_ARG;
+  if (!tensor_ok(dq) || !tensor_ok(dk) || !tensor_ok(dv)) return EA_ERR_INVALID_ARG;
+  if ((st = check_tables(res)) != EA_OK) return st;
+  if (!tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
+  ea_sizes z;
+  fill_sizes(*d, &z);
+  if (!workspace || !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
+  if (ws_bytes < z.ws_bwd) return EA_ERR_WORKSPACE;
+  return EA_OK;
+}
+
+ea_status run_bwd_stage(int stage, const Dims& d, const ea_params* params, const void* q,
+                        const void* k, const void* v, const void* dout, const ea_residuals* res,
+                        float* dq, float* dk, float* dv, void* workspace, hipStream_t s) {
+  float* delta = static_cast<float*>(workspace);
+  if (stage == 0) {
+    DeltaArgs da{dout, res->o2, delta, d.BH * d.n};
+    return from_hip(launch_delta(da, d.dtype, (int)d.d, s));
+  }
+  const float c = (params->alpha - 1.0f) * params->scale;
+  const float gamma = 1.0f / (params->alpha - 1.0f);
+  BwdArgs ba{q, k, v, dout, res->tau, delta, res->q_count, res->q_index, res->k_count,
+             res->k_index, dq, dk, dv, (int)d.BH, (int)d.n, (int)d.T, c, gamma,
+             params->scale, params->causal, gamma_kind(params->alpha)};
+  if (stage == 1) return from_hip(launch_bwd_dkdv(ba, d.dtype, (int)d.d, s));
+  return from_hip(launch_bwd_dq(ba, d.dtype, (int)d.d, s));
+}
+
+}  // namespace
+
 ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const void* q,
                           const void* k, const void* v, void* o, const ea_residuals* res,
                           void* workspace, size_t ws_bytes, void* stream) {
   (void)workspace;
   (void)ws_bytes;
   Dims d;
-  ea_status st = check_shape(shape, params, &d);
+  ea_status st = prep_fwd(shape, params, q, k, v, o, res, &d);
   if (st != EA_OK) return st;
-  if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(o)) return EA_ERR_INVALID_ARG;
-  if ((st = check_tables(res)) != EA_OK) return st;
-  if (params->need_bwd && !tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const float c = (params->alpha - 1.0f) * params->scale;
-  const float gamma = 1.0f / (params->alpha - 1.0f);
-  const int gk = gamma_kind(params->alpha);
+  for (int stage = 0; stage < 3; ++stage)
+    if ((st = run_fwd_stage(stage, d, params, q, k, v, o, res, s)) != EA_OK) return st;
+  return EA_OK;
+}
 
-  TauArgs ta{q, k, res->tau, res->block_mask, res->stats, (int)d.BH, (int)d.n, (int)d.T,
-             c, params->alpha, gamma, params->causal, params->max_iter, params->tol, gk};
-  if ((st = from_hip(launch_tau(ta, d.dtype, (int)d.d, s))) != EA_OK) return st;
-
-  CompactArgs ca{res->block_mask, res->q_count, res->q_index, res->k_count, res->k_index,
-                 (int)d.BH, (int)d.T};
-  if ((st = from_hip(launch_compact(ca, s))) != EA_OK) return st;
-
-  FwdArgs fa{q, k, v, o, params->need_bwd ? res->o2 : nullptr, res->tau, res->q_count,
-             res->q_index, (int)d.BH, (int)d.n, (int)d.T, c, gamma, params->causal, gk};
-  return from_hip(launch_fwd(fa, d.dtype, (int)d.d, params->need_bwd != 0, s));
+ea_status entmax_attn_fwd_stage(int stage, const ea_shape* shape, const ea_params* params,
+                                const void* q, const void* k, const void* v, void* o,
+                                const ea_residuals* res, void* stream) {
+  if (stage < 0 || stage > 2) return EA_ERR_INVALID_ARG;
+  Dims d;
+  ea_status st = prep_fwd(shape, params, q, k, v, o, res, &d);
+  if (st != EA_OK) return st;
+  return run_fwd_stage(stage, d, params, q, k, v, o, res, static_cast<hipStream_t>(stream));
 }
 
 ea_status entmax_attn_bwd(const ea_shape* shape, const ea_params* params, const void* q,
@@ -144,29 +209,25 @@ ea_status entmax_attn_bwd(const ea_shape* shape, const ea_params* params, const 
                           const ea_residuals* res, float* dq, float* dk, float* dv,
                           void* workspace, size_t ws_bytes, void* stream) {
   Dims d;
-  ea_status st = check_shape(shape, params, &d);
+  ea_status st = prep_bwd(shape, params, q, k, v, dout, res, dq, dk, dv, workspace, ws_bytes, &d);
   if (st != EA_OK) return st;
-  if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(dout)) return EA_ERR_INVALID_ARG;
-  if (!tensor_ok(dq) || !tensor_ok(dk) || !tensor_ok(dv)) return EA_ERR_INVALID_ARG;
-  if ((st = check_tables(res)) != EA_OK) return st;
-  if (!tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
-  ea_sizes z;
-  fill_sizes(d, &z);
-  if (!workspace || !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
-  if (ws_bytes < z.ws_bwd) return EA_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const float c = (params->alpha - 1.0f) * params->scale;
-  const float gamma = 1.0f / (params->alpha - 1.0f);
-  float* delta = static_cast<float*>(workspace);
+  for (int stage = 0; stage < 3; ++stage)
+    if ((st = run_bwd_stage(stage, d, params, q, k, v, dout, res, dq, dk, dv, workspace, s)) != EA_OK)
+      return st;
+  return EA_OK;
+}
 
-  DeltaArgs da{dout, res->o2, delta, d.BH * d.n};
-  if ((st = from_hip(launch_delta(da, d.dtype, (int)d.d, s))) != EA_OK) return st;
-
-  BwdArgs ba{q, k, v, dout, res->tau, delta, res->q_count, res->q_index, res->k_count,
-             res->k_index, dq, dk, dv, (int)d.BH, (int)d.n, (int)d.T, c, gamma,
-             params->scale, params->causal, gamma_kind(params->alpha)};
-  if ((st = from_hip(launch_bwd_dkdv(ba, d.dtype, (int)d.d, s))) != EA_OK) return st;
-  return from_hip(launch_bwd_dq(ba, d.dtype, (int)d.d, s));
+ea_status entmax_attn_bwd_stage(int stage, const ea_shape* shape, const ea_params* params,
+                                const void* q, const void* k, const void* v, const void* dout,
+                                const ea_residuals* res, float* dq, float* dk, float* dv,
+                                void* workspace, size_t ws_bytes, void* stream) {
+  if (stage < 0 || stage > 2) return EA_ERR_INVALID_ARG;
+  Dims d;
+  ea_status st = prep_bwd(shape, params, q, k, v, dout, res, dq, dk, dv, workspace, ws_bytes, &d);
+  if (st != EA_OK) return st;
+  return run_bwd_stage(stage, d, params, q, k, v, dout, res, dq, dk, dv, workspace,
+                       static_cast<hipStream_t>(stream));
 }
 
 const char* entmax_attn_status_string(ea_status s) {
