@@ -18,10 +18,13 @@
 // (hi + lo) so dK and dQ keep ~16 mantissa bits of dS; outputs are fp32.
 //
 // gfx950 layout: 2 waves per workgroup, 32 resident rows per wave in
-// registers (K and V rows for dK/dV; Q and dO rows for dQ), the other side's
-// 64-row tiles staged in LDS row-major (for S, dP) and transposed (for the
-// permuted contraction of P^T dO, dS^T Q, dS K).  No atomics: every output
-// row has one owner, so results are deterministic.
+// registers (K and V rows for dK/dV; Q and dO rows for dQ); the other side's
+// 64-row tiles are copied by global_load_lds into double-buffered row-major
+// LDS tiles, read directly for S and dP and through transposing LDS reads for
+// the permuted contractions P^T dO, dS^T Q and dS K.  No atomics: every
+// output row has one owner, so results are deterministic.
+#include <type_traits>
+
 #include "ea_common.h"
 #include "ea_internal.h"
 
@@ -54,16 +57,14 @@ __global__ __launch_bounds__(256) void delta_kernel(DeltaArgs a) {
 
 template <typename E, int D, int GK>
 __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
-  using G = TileGeom<E, D>;
+  using TL = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
   constexpr int NTD = D / 32;
   constexpr int PS = perm_steps<E>();
-  __shared__ __attribute__((aligned(16))) E q_rm[G::RM_ELEMS];
-  __shared__ __attribute__((aligned(16))) E q_tr[G::TR_ELEMS];
-  __shared__ __attribute__((aligned(16))) E do_rm[G::RM_ELEMS];
-  __shared__ __attribute__((aligned(16))) E do_tr[G::TR_ELEMS];
-  __shared__ float tau_s[BLK], del_s[BLK];
+  __shared__ __attribute__((aligned(16))) E qbuf[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) E dobuf[2][TL::ELEMS];
+  __shared__ float tau_s[2][BLK], del_s[2][BLK];
 
   const int lane = lane_id(), w = wave_id();
   const int n = a.n, T = a.T;
@@ -98,71 +99,76 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
     dv[t] = zero16();
   }
 
-  TileRegs<E, D, BWD_NT> qr, dr;
-  float tv = 0.f, dlv = 0.f;
-  auto prefetch = [&](int qb) {
-    qr.load(Qg, qb * BLK, n);
-    dr.load(dOg, qb * BLK, n);
-    if (threadIdx.x < BLK) {
-      const int r = qb * BLK + threadIdx.x;
-      tv = r < n ? taug[r] : 0.f;
-      dlv = r < n ? delg[r] : 0.f;
+  // One 32-query half of the staged block against this wave's 32 keys:
+  // S = Q K^T, dP = dO V^T (rows = queries), then dV += P^T dO, dK += dS^T Q.
+  auto block = [&](auto masked, const E* qt, const E* dt, const float* ts, const float* ds_,
+                   int qh, int i0) {
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      s = M::mma(lds_row_frag<E, D>(qt, 32 * qh + (lane & 31), kk), kf[kk], s);
+      dp = M::mma(lds_row_frag<E, D>(dt, 32 * qh + (lane & 31), kk), vf[kk], dp);
+    }
+    float p[16], dsv[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int qi = 32 * qh + crow(r);
+      float zp = relu_z(c, s[r], ts[qi]);
+      if constexpr (decltype(masked)::value) {
+        const int i = i0 + crow(r);
+        zp = (i < n && j < n && (!a.causal || j <= i)) ? zp : 0.f;
+      }
+      float u;
+      Gamma<GK>::pu(zp, g, p[r], u);
+      dsv[r] = u * (dp[r] - ds_[qi]);
+    }
+#pragma unroll
+    for (int t = 0; t < PS; ++t) {
+      const typename M::frag pa = M::pack(p, t);
+      typename M::frag dh, dl;
+      M::pack_split(dsv, t, dh, dl);
+#pragma unroll
+      for (int nt = 0; nt < NTD; ++nt) {
+        dv[nt] = M::mma(pa, lds_perm_frag<E, D>(dt, 32 * nt, 32 * qh, t), dv[nt]);
+        const typename M::frag qb_ = lds_perm_frag<E, D>(qt, 32 * nt, 32 * qh, t);
+        dk[nt] = M::mma(dh, qb_, dk[nt]);
+        if constexpr (!M::exact_operands) dk[nt] = M::mma(dl, qb_, dk[nt]);
+      }
     }
   };
-  if (cnt > 0) prefetch(list[0]);
-  for (int e = 0; e < cnt; ++e) {
+
+  float tv = 0.f, dlv = 0.f;
+  auto issue = [&](int e) {
     const int qb = list[e];
-    __syncthreads();
-    qr.store_rm(q_rm);
-    qr.store_tr(q_tr);
-    dr.store_rm(do_rm);
-    dr.store_tr(do_tr);
+    tile_dma<E, D, BWD_NT>(qbuf[e & 1], Qg, qb * BLK, n);
+    tile_dma<E, D, BWD_NT>(dobuf[e & 1], dOg, qb * BLK, n);
     if (threadIdx.x < BLK) {
-      tau_s[threadIdx.x] = tv;
-      del_s[threadIdx.x] = dlv;
+      const int r = min(qb * BLK + (int)threadIdx.x, n - 1);
+      tv = taug[r];
+      dlv = delg[r];
+    }
+  };
+  if (cnt > 0) issue(0);
+  for (int e = 0; e < cnt; ++e) {
+    dma_wait();
+    if (threadIdx.x < BLK) {
+      tau_s[e & 1][threadIdx.x] = tv;
+      del_s[e & 1][threadIdx.x] = dlv;
     }
     __syncthreads();
-    if (e + 1 < cnt) prefetch(list[e + 1]);
+    const int qb = list[e];
+    if (e + 1 < cnt) issue(e + 1);
     if (!wave_ok) continue;
+    const E* qt = qbuf[e & 1];
+    const E* dt = dobuf[e & 1];
 #pragma unroll
     for (int qh = 0; qh < 2; ++qh) {
       const int i0 = qb * BLK + 32 * qh;
       if (i0 >= n || (a.causal && k0 > i0 + 31)) continue;
-      const bool edge = i0 + 31 >= n || k0 + 31 >= n || (a.causal && k0 + 31 > i0);
-      // S = Q K^T and dP = dO V^T, rows = queries, columns = this wave's keys
-      f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        s = M::mma(lds_row_frag<E, D>(q_rm, 32 * qh + (lane & 31), kk), kf[kk], s);
-        dp = M::mma(lds_row_frag<E, D>(do_rm, 32 * qh + (lane & 31), kk), vf[kk], dp);
-      }
-      float p[16], ds[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int qi = 32 * qh + crow(r);
-        float zp = relu_z(c, s[r], tau_s[qi]);
-        if (edge) {
-          const int i = qb * BLK + qi;
-          if (i >= n || j >= n || (a.causal && j > i)) zp = 0.f;
-        }
-        float u;
-        Gamma<GK>::pu(zp, g, p[r], u);
-        ds[r] = u * (dp[r] - del_s[qi]);
-      }
-#pragma unroll
-      for (int t = 0; t < PS; ++t) {
-        const typename M::frag pa = M::pack(p, t);
-        typename M::frag dh, dl;
-        M::pack_split(ds, t, dh, dl);
-#pragma unroll
-        for (int nt = 0; nt < NTD; ++nt) {
-          const int col = 32 * nt + (lane & 31);
-          dv[nt] = M::mma(pa, lds_perm_frag<E>(do_tr, col, 32 * qh, t), dv[nt]);
-          const typename M::frag qb_ = lds_perm_frag<E>(q_tr, col, 32 * qh, t);
-          dk[nt] = M::mma(dh, qb_, dk[nt]);
-          if constexpr (!M::exact_operands) dk[nt] = M::mma(dl, qb_, dk[nt]);
-        }
-      }
+      if (i0 + 31 >= n || k0 + 31 >= n || (a.causal && k0 + 31 > i0))
+        block(std::true_type{}, qt, dt, tau_s[e & 1], del_s[e & 1], qh, i0);
+      else
+        block(std::false_type{}, qt, dt, tau_s[e & 1], del_s[e & 1], qh, i0);
     }
   }
 
@@ -187,14 +193,13 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
 
 template <typename E, int D, int GK>
 __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
-  using G = TileGeom<E, D>;
+  using TL = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
   constexpr int NTD = D / 32;
   constexpr int PS = perm_steps<E>();
-  __shared__ __attribute__((aligned(16))) E k_rm[G::RM_ELEMS];
-  __shared__ __attribute__((aligned(16))) E k_tr[G::TR_ELEMS];
-  __shared__ __attribute__((aligned(16))) E v_rm[G::RM_ELEMS];
+  __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) E vbuf[2][TL::ELEMS];
 
   const int lane = lane_id(), w = wave_id();
   const int n = a.n, T = a.T;
@@ -204,6 +209,7 @@ __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
   const int q0 = qb * BLK + 32 * w;
   const int i = q0 + (lane & 31);
   const bool wave_ok = q0 < n;
+  const int wave_last = min(n - 1, q0 + 31);
   const size_t head = (size_t)bh * n * D;
   const E* Qg = static_cast<const E*>(a.q) + head;
   const E* Kg = static_cast<const E*>(a.k) + head;
@@ -227,58 +233,63 @@ __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
 #pragma unroll
   for (int t = 0; t < NTD; ++t) dq[t] = zero16();
 
-  TileRegs<E, D, BWD_NT> kr, vr;
-  if (cnt > 0) {
-    kr.load(Kg, list[0] * BLK, n);
-    vr.load(Vg, list[0] * BLK, n);
-  }
-  for (int e = 0; e < cnt; ++e) {
+  auto sub_kind = [&](int j0) {
+    if (!wave_ok || j0 >= n || (a.causal && j0 > wave_last)) return 0;
+    if (j0 + 31 >= n || (a.causal && j0 + 31 > q0)) return 2;
+    return 1;
+  };
+  // One 32-key half of the staged block: S^T = K Q^T, dP^T = V dO^T
+  // (rows = keys, columns = this wave's queries), then dQ += dS K.
+  auto block = [&](auto masked, const E* kt, const E* vt, int sub, int j0) {
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      s = M::mma(lds_row_frag<E, D>(kt, 32 * sub + (lane & 31), kk), qf[kk], s);
+      dp = M::mma(lds_row_frag<E, D>(vt, 32 * sub + (lane & 31), kk), df[kk], dp);
+    }
+    float dsv[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float zp = relu_z(c, s[r], tau);
+      if constexpr (decltype(masked)::value) {
+        const int jj = j0 + crow(r);
+        zp = (jj < n && (!a.causal || jj <= i)) ? zp : 0.f;
+      }
+      float p, u;
+      Gamma<GK>::pu(zp, g, p, u);
+      dsv[r] = u * (dp[r] - del);
+    }
+#pragma unroll
+    for (int t = 0; t < PS; ++t) {
+      typename M::frag dh, dl;
+      M::pack_split(dsv, t, dh, dl);
+#pragma unroll
+      for (int nt = 0; nt < NTD; ++nt) {
+        const typename M::frag kb_ = lds_perm_frag<E, D>(kt, 32 * nt, 32 * sub, t);
+        dq[nt] = M::mma(dh, kb_, dq[nt]);
+        if constexpr (!M::exact_operands) dq[nt] = M::mma(dl, kb_, dq[nt]);
+      }
+    }
+  };
+
+  auto issue = [&](int e) {
     const int kb = list[e];
+    tile_dma<E, D, BWD_NT>(kbuf[e & 1], Kg, kb * BLK, n);
+    tile_dma<E, D, BWD_NT>(vbuf[e & 1], Vg, kb * BLK, n);
+  };
+  if (cnt > 0) issue(0);
+  for (int e = 0; e < cnt; ++e) {
+    dma_wait();
     __syncthreads();
-    kr.store_rm(k_rm);
-    kr.store_tr(k_tr);
-    vr.store_rm(v_rm);
-    __syncthreads();
-    if (e + 1 < cnt) {
-      kr.load(Kg, list[e + 1] * BLK, n);
-      vr.load(Vg, list[e + 1] * BLK, n);
-    }
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      const int j0 = kb * BLK + 32 * sub;
-      if (!wave_ok || j0 >= n || (a.causal && j0 > min(n - 1, q0 + 31))) continue;
-      const bool edge = j0 + 31 >= n || (a.causal && j0 + 31 > q0);
-      // S^T = K Q^T and dP^T = V dO^T: rows = keys, columns = this wave's queries
-      f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        s = M::mma(lds_row_frag<E, D>(k_rm, 32 * sub + (lane & 31), kk), qf[kk], s);
-        dp = M::mma(lds_row_frag<E, D>(v_rm, 32 * sub + (lane & 31), kk), df[kk], dp);
-      }
-      float ds[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float zp = relu_z(c, s[r], tau);
-        if (edge) {
-          const int jj = j0 + crow(r);
-          if (jj >= n || (a.causal && jj > i)) zp = 0.f;
-        }
-        float p, u;
-        Gamma<GK>::pu(zp, g, p, u);
-        ds[r] = u * (dp[r] - del);
-      }
-#pragma unroll
-      for (int t = 0; t < PS; ++t) {
-        typename M::frag dh, dl;
-        M::pack_split(ds, t, dh, dl);
-#pragma unroll
-        for (int nt = 0; nt < NTD; ++nt) {
-          const typename M::frag kb_ = lds_perm_frag<E>(k_tr, 32 * nt + (lane & 31), 32 * sub, t);
-          dq[nt] = M::mma(dh, kb_, dq[nt]);
-          if constexpr (!M::exact_operands) dq[nt] = M::mma(dl, kb_, dq[nt]);
-        }
-      }
-    }
+    if (e + 1 < cnt) issue(e + 1);
+    const E* kt = kbuf[e & 1];
+    const E* vt = vbuf[e & 1];
+    const int j0 = list[e] * BLK;
+    const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
+    if (k0 == 1) block(std::false_type{}, kt, vt, 0, j0);
+    else if (k0 == 2) block(std::true_type{}, kt, vt, 0, j0);
+    if (k1 == 1) block(std::false_type{}, kt, vt, 1, j0 + 32);
+    else if (k1 == 2) block(std::true_type{}, kt, vt, 1, j0 + 32);
   }
 
   if (!wave_ok) return;

@@ -135,109 +135,103 @@ __device__ __forceinline__ typename Mma<E>::frag load_row_frag_global(const E* b
 
 // -------------------------------------------------------------- LDS tiles
 //
-// A 64 x D tile of a [*, D] row-major global matrix, staged in LDS in up to
-// two layouts:
-//   row-major   rm[r * RP + c]            RP = D + 16 bytes of padding
-//   transposed  tr[c * 64 + swz(c, r)]    r = tile row, XOR-swizzled in groups
-//                                         of 4 so that both the transposing
-//                                         stores and the 8-byte permuted reads
-//                                         spread over the LDS banks.
-// Loading goes through registers (16-byte global loads, consecutive threads
-// on consecutive 16-byte chunks of a row) so the next tile can be in flight
-// while the current one is consumed.
+// A 64 x D tile of a [*, D] row-major global matrix is staged in LDS
+// row-major in 16-byte chunks, chunk (r, c) of tile row r stored at chunk
+// position r * CPR + (c ^ (r % CPR)) (CPR chunks per row).  The XOR swizzle
+// spreads both access patterns over the banks: 32 lanes reading one chunk
+// column of 32 rows (MFMA row fragments), and the 8-row x 32-column blocks
+// read by the transposing loads.
+//
+// Tiles are filled with global_load_lds (16 bytes per lane, written to LDS
+// without passing through registers): wave instruction k writes chunk
+// positions [64k, 64k + 64), so each lane fetches the global chunk whose
+// swizzled position it owns.  Rows past the end of the matrix repeat its
+// last row; every kernel masks those rows' contributions to exactly zero.
+// Completion is awaited with dma_wait() followed by a workgroup barrier.
 
 template <typename E, int D>
-struct TileGeom {
-  static constexpr int VEC = 16 / (int)sizeof(E);        // elements per 16-byte chunk
-  static constexpr int CPR = D / VEC;                    // chunks per row
-  static constexpr int CHUNKS = BLK * CPR;               // chunks per tile
-  static constexpr int RP = D + VEC;                     // row-major pitch (elements)
-  static constexpr int RM_ELEMS = BLK * RP;
-  static constexpr int TR_ELEMS = D * BLK;
+struct Tile {
+  static constexpr int VEC = 16 / (int)sizeof(E);  // elements per 16-byte chunk
+  static constexpr int CPR = D / VEC;              // chunks per row
+  static constexpr int CHUNKS = BLK * CPR;
+  static constexpr int ELEMS = BLK * D;
+  __device__ __forceinline__ static int chunk_pos(int r, int c) { return r * CPR + (c ^ (r & (CPR - 1))); }
+  // element offset of (row r, column col)
+  __device__ __forceinline__ static int elem(int r, int col) {
+    return chunk_pos(r, col / VEC) * VEC + (col & (VEC - 1));
+  }
 };
 
-__device__ __forceinline__ int tr_swz(int c, int r) {
-  return r ^ ((((c ^ (c >> 3)) & 15)) << 2);
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+
+__device__ __forceinline__ lds_void_t* to_lds(const void* p) {
+  return (lds_void_t*)((__attribute__((address_space(3))) char*)(p));
 }
 
+// Asynchronous copy of tile rows [row0, row0 + 64) of g ([nrows, D]) into
+// `tile`, spread over the NT threads of the workgroup.
 template <typename E, int D, int NT>
-struct TileRegs {
-  static constexpr int PER = TileGeom<E, D>::CHUNKS / NT;
-  static_assert(TileGeom<E, D>::CHUNKS % NT == 0, "tile chunks must divide the workgroup");
-  u32x4 v[PER];
-
-  // Load tile rows [row0, row0 + 64) of a matrix with `nrows` rows; rows past
-  // the end are zero.
-  __device__ __forceinline__ void load(const E* base, int row0, int nrows) {
-    constexpr int CPR = TileGeom<E, D>::CPR, VEC = TileGeom<E, D>::VEC;
+__device__ __forceinline__ void tile_dma(E* tile, const E* g, int row0, int nrows) {
+  using TL = Tile<E, D>;
+  constexpr int INSTR = TL::CHUNKS / 64;
+  constexpr int NW = NT / 64;
+  static_assert(INSTR % NW == 0, "tile instructions must divide the waves");
+#if defined(__HIP_DEVICE_COMPILE__)  // gfx950 builtin; kernels' lambdas are also parsed for the host
+  const int l = lane_id();
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int q = threadIdx.x + NT * i;
-      const int r = q / CPR, c = q % CPR;
-      const int row = row0 + r;
-      u32x4 x = {0u, 0u, 0u, 0u};
-      if (row < nrows) x = *reinterpret_cast<const u32x4*>(base + (size_t)row * D + c * VEC);
-      v[i] = x;
-    }
+  for (int k0 = 0; k0 < INSTR; k0 += NW) {
+    const int k = k0 + wave_id();
+    const int p = 64 * k + l;
+    const int r = p / TL::CPR;
+    const int c = (p % TL::CPR) ^ (r & (TL::CPR - 1));
+    const int row = min(row0 + r, nrows - 1);
+    __builtin_amdgcn_global_load_lds(g + (size_t)row * D + c * TL::VEC, to_lds(tile + 64 * k * TL::VEC),
+                                     16, 0, 0);
   }
+#endif
+}
 
-  __device__ __forceinline__ void store_rm(E* rm) const {
-    constexpr int CPR = TileGeom<E, D>::CPR, VEC = TileGeom<E, D>::VEC, RP = TileGeom<E, D>::RP;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int q = threadIdx.x + NT * i;
-      const int r = q / CPR, c = q % CPR;
-      *reinterpret_cast<u32x4*>(rm + r * RP + c * VEC) = v[i];
-    }
-  }
+// Waits for this wave's outstanding global loads, global_load_lds included
+// (s_waitcnt vmcnt(0)); follow with a barrier before reading the tiles.
+__device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-  __device__ __forceinline__ void store_tr(E* tr) const {
-    constexpr int CPR = TileGeom<E, D>::CPR, VEC = TileGeom<E, D>::VEC;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int q = threadIdx.x + NT * i;
-      const int r = q / CPR, c0 = (q % CPR) * VEC;
-      if constexpr (sizeof(E) == 2) {
-        const uint16_t* s = reinterpret_cast<const uint16_t*>(&v[i]);
-        uint16_t* t = reinterpret_cast<uint16_t*>(tr);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) t[(c0 + e) * BLK + tr_swz(c0 + e, r)] = s[e];
-      } else {
-        const float* s = reinterpret_cast<const float*>(&v[i]);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) tr[(c0 + e) * BLK + tr_swz(c0 + e, r)] = s[e];
-      }
-    }
-  }
-};
-
-// A-operand row fragment from a row-major LDS tile: tile row `r`, k step kk.
+// A-operand row fragment of tile row r, k step kk.
 template <typename E, int D>
-__device__ __forceinline__ typename Mma<E>::frag lds_row_frag(const E* rm, int r, int kk) {
-  constexpr int RP = TileGeom<E, D>::RP;
+__device__ __forceinline__ typename Mma<E>::frag lds_row_frag(const E* tile, int r, int kk) {
+  using TL = Tile<E, D>;
   const int h = lane_id() >> 5;
   if constexpr (Mma<E>::EPL == 8) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(rm + r * RP + 16 * kk + 8 * h));
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(tile + TL::chunk_pos(r, 2 * kk + h) * 8));
   } else {
-    return rm[r * RP + 2 * kk + h];
+    return tile[TL::elem(r, 2 * kk + h)];
   }
 }
 
 // B-operand fragment for the permuted contraction over tile rows
-// [rbase, rbase + 32): column `c` of the tile (an index in 0..D-1), step t.
-template <typename E>
-__device__ __forceinline__ typename Mma<E>::frag lds_perm_frag(const E* tr, int c, int rbase, int t) {
-  const int h = lane_id() >> 5;
+// [rbase, rbase + 32), output column cbase + l % 32, step t.  bf16: two
+// transposing reads (ds_read_b64_tr_b16): in each 16-lane group, lane j
+// addresses row r0 + j/4, columns 4 (j % 4) .. +3 of a 16-column strip, and
+// lane i receives column i of the four rows r0 .. r0 + 3.
+template <typename E, int D>
+__device__ __forceinline__ typename Mma<E>::frag lds_perm_frag(const E* tile, int cbase, int rbase, int t) {
+  using TL = Tile<E, D>;
+  const int l = lane_id();
   if constexpr (Mma<E>::EPL == 8) {
-    const int r0 = rbase + 16 * t + 4 * h;  // rows r0..r0+3 and r0+8..r0+11
-    const E* col = tr + c * BLK;
-    u32x2 a = *reinterpret_cast<const u32x2*>(col + tr_swz(c, r0));
-    u32x2 b = *reinterpret_cast<const u32x2*>(col + tr_swz(c, r0 + 8));
-    u32x4 v = {a.x, a.y, b.x, b.y};
+#if defined(__HIP_DEVICE_COMPILE__)
+    const int r0 = rbase + 16 * t + 4 * (l >> 5) + ((l & 15) >> 2);
+    const int col = cbase + 16 * ((l >> 4) & 1) + 4 * (l & 3);
+    const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)to_lds(tile + TL::elem(r0, col)));
+    const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)to_lds(tile + TL::elem(r0 + 8, col)));
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const s16x8 v = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
     return __builtin_bit_cast(bf16x8, v);
+#else
+    return bf16x8{};
+#endif
   } else {
-    const int r = rbase + 8 * (t >> 2) + 4 * h + (t & 3);
-    return tr[c * BLK + tr_swz(c, r)];
+    return tile[TL::elem(rbase + perm_key<E>(t, 0), cbase + (l & 31))];
   }
 }
 

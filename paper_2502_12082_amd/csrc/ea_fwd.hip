@@ -16,9 +16,13 @@
 // gfx950 layout: one workgroup = 2 waves = one 64-row query block; each wave
 // holds 32 query rows as MFMA B operands, computes S^T (keys x queries) so the
 // probabilities come out with one query per lane, and feeds them back as the
-// A operand of P V with a permuted contraction order (see ea_common.h).  K is
-// staged row-major and V transposed in LDS; the next listed block is loaded
-// into registers while the current one is consumed.
+// A operand of P V with a permuted contraction order (see ea_common.h).  K and
+// V blocks are copied into double-buffered LDS tiles by global_load_lds (the
+// next listed block in flight while the current one is consumed); V's
+// operand fragments come out of its row-major tile through transposing LDS
+// reads.
+#include <type_traits>
+
 #include "ea_common.h"
 #include "ea_internal.h"
 
@@ -60,13 +64,13 @@ constexpr int FWD_NT = 128;
 
 template <typename E, int D, int GK, bool TRAIN>
 __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
-  using G = TileGeom<E, D>;
+  using TL = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
   constexpr int NTD = D / 32;
   constexpr int PS = perm_steps<E>();
-  __shared__ __attribute__((aligned(16))) E k_rm[G::RM_ELEMS];
-  __shared__ __attribute__((aligned(16))) E v_tr[G::TR_ELEMS];
+  __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) E vbuf[2][TL::ELEMS];
 
   const int lane = lane_id(), w = wave_id();
   const int n = a.n, T = a.T;
@@ -76,6 +80,7 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
   const int q0 = qb * BLK + 32 * w;
   const int i = q0 + (lane & 31);
   const bool wave_ok = q0 < n;
+  const int wave_last = min(n - 1, q0 + 31);
   const size_t head = (size_t)bh * n * D;
   const E* Q = static_cast<const E*>(a.q) + head;
   const E* K = static_cast<const E*>(a.k) + head;
@@ -98,61 +103,72 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
   }
   float usum = 0.f;
 
-  TileRegs<E, D, FWD_NT> kr, vr;
-  if (cnt > 0) {
-    kr.load(K, list[0] * BLK, n);
-    vr.load(V, list[0] * BLK, n);
-  }
-  for (int e = 0; e < cnt; ++e) {
-    const int kb = list[e];
-    __syncthreads();
-    kr.store_rm(k_rm);
-    vr.store_tr(v_tr);
-    __syncthreads();
-    if (e + 1 < cnt) {
-      kr.load(K, list[e + 1] * BLK, n);
-      vr.load(V, list[e + 1] * BLK, n);
+  // 0 = no valid key for this wave, 1 = all valid, 2 = per-element masking
+  auto sub_kind = [&](int j0) {
+    if (!wave_ok || j0 >= n || (a.causal && j0 > wave_last)) return 0;
+    if (j0 + 31 >= n || (a.causal && j0 + 31 > q0)) return 2;
+    return 1;
+  };
+  // P (and U) of one 32-key sub-tile, then O += P V (and U V into O2).
+  auto apply = [&](auto masked, const f32x16& s, const E* vt, int sub, int j0) {
+    float p[16], u[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float zp = relu_z(c, s[r], tau);
+      if constexpr (decltype(masked)::value) {
+        const int j = j0 + crow(r);
+        zp = (j < n && (!a.causal || j <= i)) ? zp : 0.f;
+      }
+      if constexpr (TRAIN) {
+        Gamma<GK>::pu(zp, g, p[r], u[r]);
+        usum += u[r];
+      } else {
+        p[r] = Gamma<GK>::p_only(zp, g);
+      }
     }
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      const int j0 = kb * BLK + 32 * sub;
-      if (!wave_ok || j0 >= n || (a.causal && j0 > min(n - 1, q0 + 31))) continue;
-      const bool edge = j0 + 31 >= n || (a.causal && j0 + 31 > q0);
-      f32x16 s = zero16();
+    for (int t = 0; t < PS; ++t) {
+      const typename M::frag pa = M::pack(p, t);
+      typename M::frag uh, ul;
+      if constexpr (TRAIN) M::pack_split(u, t, uh, ul);
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-        s = M::mma(lds_row_frag<E, D>(k_rm, 32 * sub + (lane & 31), kk), qf[kk], s);
-      float p[16], u[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float zp = relu_z(c, s[r], tau);
-        if (edge) {
-          const int j = j0 + crow(r);
-          if (j >= n || (a.causal && j > i)) zp = 0.f;
-        }
+      for (int nt = 0; nt < NTD; ++nt) {
+        const typename M::frag vb = lds_perm_frag<E, D>(vt, 32 * nt, 32 * sub, t);
+        o[nt] = M::mma(pa, vb, o[nt]);
         if constexpr (TRAIN) {
-          Gamma<GK>::pu(zp, g, p[r], u[r]);
-          usum += u[r];
-        } else {
-          p[r] = Gamma<GK>::p_only(zp, g);
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < PS; ++t) {
-        const typename M::frag pa = M::pack(p, t);
-        typename M::frag uh, ul;
-        if constexpr (TRAIN) M::pack_split(u, t, uh, ul);
-#pragma unroll
-        for (int nt = 0; nt < NTD; ++nt) {
-          const typename M::frag vb = lds_perm_frag<E>(v_tr, 32 * nt + (lane & 31), 32 * sub, t);
-          o[nt] = M::mma(pa, vb, o[nt]);
-          if constexpr (TRAIN) {
-            o2[nt] = M::mma(uh, vb, o2[nt]);
-            if constexpr (!M::exact_operands) o2[nt] = M::mma(ul, vb, o2[nt]);
-          }
+          o2[nt] = M::mma(uh, vb, o2[nt]);
+          if constexpr (!M::exact_operands) o2[nt] = M::mma(ul, vb, o2[nt]);
         }
       }
     }
+  };
+
+  auto issue = [&](int e) {
+    const int kb = list[e];
+    tile_dma<E, D, FWD_NT>(kbuf[e & 1], K, kb * BLK, n);
+    tile_dma<E, D, FWD_NT>(vbuf[e & 1], V, kb * BLK, n);
+  };
+  if (cnt > 0) issue(0);
+  for (int e = 0; e < cnt; ++e) {
+    dma_wait();
+    __syncthreads();
+    if (e + 1 < cnt) issue(e + 1);
+    const E* kt = kbuf[e & 1];
+    const E* vt = vbuf[e & 1];
+    const int j0 = list[e] * BLK;
+    const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
+    if (k0 == 0 && k1 == 0) continue;
+    // S^T = K Q^T for both 32-key halves, two interleaved MFMA chains
+    f32x16 s0 = zero16(), s1 = zero16();
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      if (k0) s0 = M::mma(lds_row_frag<E, D>(kt, lane & 31, kk), qf[kk], s0);
+      if (k1) s1 = M::mma(lds_row_frag<E, D>(kt, 32 + (lane & 31), kk), qf[kk], s1);
+    }
+    if (k0 == 1) apply(std::false_type{}, s0, vt, 0, j0);
+    else if (k0 == 2) apply(std::true_type{}, s0, vt, 0, j0);
+    if (k1 == 1) apply(std::false_type{}, s1, vt, 1, j0 + 32);
+    else if (k1 == 2) apply(std::true_type{}, s1, vt, 1, j0 + 32);
   }
 
   if (!wave_ok) return;

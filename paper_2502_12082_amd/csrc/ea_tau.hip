@@ -17,8 +17,11 @@
 // rows); each wave keeps its 32 query rows as MFMA B operands in registers
 // and computes S^T tiles (keys x queries), so every lane owns one query and
 // the per-row sums stay in-lane until the end of a pass.  K tiles of 64 keys
-// go through LDS, the next one in flight in registers.  A workgroup stops as
+// are copied into a double-buffered LDS tile by global_load_lds, the next
+// one in flight while the current one is consumed.  A workgroup stops as
 // soon as every row it owns has |f(tau)| <= tol, or after max_iter updates.
+#include <type_traits>
+
 #include "ea_common.h"
 #include "ea_internal.h"
 
@@ -32,10 +35,10 @@ constexpr int TAU_ROWS = 32 * TAU_WAVES;
 
 template <typename E, int D, int GK>
 __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
-  using G = TileGeom<E, D>;
+  using TL = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
-  __shared__ __attribute__((aligned(16))) E k_rm[G::RM_ELEMS];
+  __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
   __shared__ uint8_t bits[TAU_WAVES * MAX_KEY_BLOCKS];
 
   const int lane = lane_id(), w = wave_id();
@@ -65,28 +68,41 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
 
   const float c = a.c;
 
-  // Streams every key block the workgroup needs; `body(kb)` sees K block kb
-  // in k_rm.
+  // Streams every key block the workgroup needs, double-buffered: block
+  // kb + 1 is copied into LDS while `body(kb, tile)` works on block kb.
   auto stream = [&](auto&& body) {
-    TileRegs<E, D, TAU_NT> regs;
-    regs.load(K, 0, n);
+    tile_dma<E, D, TAU_NT>(kbuf[0], K, 0, n);
     for (int kb = 0; kb < nkb; ++kb) {
+      dma_wait();
       __syncthreads();
-      regs.store_rm(k_rm);
-      __syncthreads();
-      if (kb + 1 < nkb) regs.load(K, (kb + 1) * BLK, n);
-      body(kb);
+      if (kb + 1 < nkb) tile_dma<E, D, TAU_NT>(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
+      body(kb, kbuf[kb & 1]);
     }
+    __syncthreads();  // the next pass refills buffer 0
   };
 
-  // S^T sub-tile: keys [32 sub, 32 sub + 32) of the staged block x this
+  // S^T sub-tiles of the staged block: keys [0, 32) and [32, 64) x this
   // wave's 32 queries; value r of lane l is key 32 sub + crow(r), query l%32.
-  auto scores = [&](int sub) {
-    f32x16 acc = zero16();
+  // The two accumulation chains are interleaved so neither waits on the other.
+  auto scores = [&](const E* kt, bool need0, bool need1, f32x16& s0, f32x16& s1) {
+    s0 = zero16();
+    s1 = zero16();
+    if (need0 && need1) {
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk)
-      acc = M::mma(lds_row_frag<E, D>(k_rm, 32 * sub + (lane & 31), kk), qf[kk], acc);
-    return acc;
+      for (int kk = 0; kk < KS; ++kk) {
+        const typename M::frag a0 = lds_row_frag<E, D>(kt, (lane & 31), kk);
+        const typename M::frag a1 = lds_row_frag<E, D>(kt, 32 + (lane & 31), kk);
+        s0 = M::mma(a0, qf[kk], s0);
+        s1 = M::mma(a1, qf[kk], s1);
+      }
+    } else if (need0) {
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) s0 = M::mma(lds_row_frag<E, D>(kt, (lane & 31), kk), qf[kk], s0);
+    } else if (need1) {
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+        s1 = M::mma(lds_row_frag<E, D>(kt, 32 + (lane & 31), kk), qf[kk], s1);
+    }
   };
   // Sub-tile state for the calling wave: 0 = nothing valid, 1 = all valid,
   // 2 = needs per-element masking (ragged tail or causal diagonal).
@@ -95,27 +111,29 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
     if (j0 + 31 >= n || (a.causal && j0 + 31 > q0)) return 2;
     return 1;
   };
+  auto valid = [&](int j) { return j < n && (!a.causal || j <= i); };
 
   // ---- pass 0: row maximum of the raw scores (scale > 0, so the maximum of
   // x = c s is c times the maximum of s)
   float smax = -INFINITY;
-  stream([&](int kb) {
+  auto max_tile = [&](auto masked, const f32x16& s, int j0) {
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      const int j0 = kb * BLK + 32 * sub;
-      const int kind = sub_kind(j0);
-      if (kind == 0) continue;
-      f32x16 s = scores(sub);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = s[r];
-        if (kind == 2) {
-          const int j = j0 + crow(r);
-          if (j >= n || (a.causal && j > i)) v = -INFINITY;
-        }
-        smax = fmaxf(smax, v);
-      }
+    for (int r = 0; r < 16; ++r) {
+      float v = s[r];
+      if constexpr (decltype(masked)::value) v = valid(j0 + crow(r)) ? v : -INFINITY;
+      smax = fmaxf(smax, v);
     }
+  };
+  stream([&](int kb, const E* kt) {
+    const int j0 = kb * BLK;
+    const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
+    if (k0 == 0 && k1 == 0) return;
+    f32x16 s0, s1;
+    scores(kt, k0 != 0, k1 != 0, s0, s1);
+    if (k0 == 1) max_tile(std::false_type{}, s0, j0);
+    else if (k0 == 2) max_tile(std::true_type{}, s0, j0);
+    if (k1 == 1) max_tile(std::false_type{}, s1, j0 + 32);
+    else if (k1 == 2) max_tile(std::true_type{}, s1, j0 + 32);
   });
   smax = fmaxf(smax, __shfl_xor(smax, 32));
 
@@ -131,75 +149,76 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
   int passes = 1;
   for (int it = 0;; ++it) {
     // ---- evaluation pass at tau: s0 = sum z^gamma, s1 = sum z^(gamma-1),
-    // s2 = sum z^(gamma-2) over the strict support z > 0
-    float s0 = 0.f, s1 = 0.f, s2 = 0.f;
-    stream([&](int kb) {
-      unsigned long long hit = 0ull;
-      bool touched = false;
+    // s2 = sum z^(gamma-2) over the strict support z > 0; for gamma = 1, 2 the
+    // count of the support is accumulated as sum ceil(z) (z is in [0, 1]).
+    float m0 = 0.f, m1 = 0.f, m2 = 0.f;
+    // Adds one sub-tile; returns whether it holds a positive probability.
+    auto eval_tile = [&](auto masked, const f32x16& s, int j0) {
+      float t0 = 0.f, t1 = 0.f, t2 = 0.f;
 #pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        const int j0 = kb * BLK + 32 * sub;
-        const int kind = sub_kind(j0);
-        if (kind == 0) continue;
-        touched = true;
-        f32x16 s = scores(sub);
-        float t0 = 0.f, t1 = 0.f, t2 = 0.f, any = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float zp = relu_z(c, s[r], tau);
-          if (kind == 2) {
-            const int j = j0 + crow(r);
-            if (j >= n || (a.causal && j > i)) zp = 0.f;
-          }
-          if constexpr (GK == 1) {
-            t0 += zp;
-            t1 += zp > 0.f ? 1.f : 0.f;
-          } else if constexpr (GK == 2) {
-            t0 = fmaf(zp, zp, t0);
-            t1 += zp;
-            t2 += zp > 0.f ? 1.f : 0.f;
-          } else if constexpr (GK == 4) {
-            const float z2 = zp * zp;
-            t0 = fmaf(z2, z2, t0);
-            t1 = fmaf(z2, zp, t1);
-            t2 += z2;
-          } else {
-            if (zp > 0.f) {
-              const float l = __log2f(zp);
-              t0 += exp2f(g * l);
-              t1 += exp2f((g - 1.f) * l);
-              t2 += exp2f((g - 2.f) * l);
-              any += 1.f;
-            }
+      for (int r = 0; r < 16; ++r) {
+        float zp = relu_z(c, s[r], tau);
+        if constexpr (decltype(masked)::value) zp = valid(j0 + crow(r)) ? zp : 0.f;
+        if constexpr (GK == 1) {
+          t0 += zp;
+          t1 += ceilf(zp);
+        } else if constexpr (GK == 2) {
+          t0 = fmaf(zp, zp, t0);
+          t1 += zp;
+          t2 += ceilf(zp);
+        } else if constexpr (GK == 4) {
+          const float z2 = zp * zp;
+          t0 = fmaf(z2, z2, t0);
+          t1 = fmaf(z2, zp, t1);
+          t2 += z2;
+        } else {
+          if (zp > 0.f) {
+            const float l = __log2f(zp);
+            t0 += exp2f(g * l);
+            t1 += exp2f((g - 1.f) * l);
+            t2 += exp2f((g - 2.f) * l);
           }
         }
-        s0 += t0;
-        s1 += t1;
-        s2 += t2;
-        const float ind = GK == 1 ? t1 : (GK == 0 ? any : t2);
-        hit |= __ballot(ind > 0.f);
       }
-      if (touched && lane == 0) bits[w * MAX_KEY_BLOCKS + kb] = hit != 0ull;
+      m0 += t0;
+      m1 += t1;
+      m2 += t2;
+      if constexpr (GK == 0) return t0 > 0.f;
+      else return (GK == 1 ? t1 : t2) > 0.f;
+    };
+    stream([&](int kb, const E* kt) {
+      const int j0 = kb * BLK;
+      const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
+      if (k0 == 0 && k1 == 0) return;
+      f32x16 s0, s1;
+      scores(kt, k0 != 0, k1 != 0, s0, s1);
+      bool any = false;
+      if (k0 == 1) any |= eval_tile(std::false_type{}, s0, j0);
+      else if (k0 == 2) any |= eval_tile(std::true_type{}, s0, j0);
+      if (k1 == 1) any |= eval_tile(std::false_type{}, s1, j0 + 32);
+      else if (k1 == 2) any |= eval_tile(std::true_type{}, s1, j0 + 32);
+      const unsigned long long hit = __ballot(any);
+      if (lane == 0) bits[w * MAX_KEY_BLOCKS + kb] = hit != 0ull;
     });
     ++passes;
-    s0 += __shfl_xor(s0, 32);
-    s1 += __shfl_xor(s1, 32);
-    s2 += __shfl_xor(s2, 32);
+    m0 += __shfl_xor(m0, 32);
+    m1 += __shfl_xor(m1, 32);
+    m2 += __shfl_xor(m2, 32);
 
-    const float f = s0 - 1.f;                        // Eq. 3
+    const float f = m0 - 1.f;                        // Eq. 3
     float f1, f2;                                    // Eq. 6, 7
     if constexpr (GK == 1) {
-      f1 = -s1;
+      f1 = -m1;
       f2 = 0.f;
     } else if constexpr (GK == 2) {
-      f1 = -2.f * s1;
-      f2 = 2.f * s2;
+      f1 = -2.f * m1;
+      f2 = 2.f * m2;
     } else if constexpr (GK == 4) {
-      f1 = -4.f * s1;
-      f2 = 12.f * s2;
+      f1 = -4.f * m1;
+      f2 = 12.f * m2;
     } else {
-      f1 = -g * s1;
-      f2 = g * (g - 1.f) * s2;
+      f1 = -g * m1;
+      f2 = g * (g - 1.f) * m2;
     }
     const bool conv = !row_ok || fabsf(f) <= a.tol;
     if (__syncthreads_and(conv) || it >= a.max_iter) break;
