@@ -64,7 +64,8 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
   constexpr int PS = perm_steps<E>();
   __shared__ __attribute__((aligned(16))) E qbuf[2][TL::ELEMS];
   __shared__ __attribute__((aligned(16))) E dobuf[2][TL::ELEMS];
-  __shared__ float tau_s[2][BLK], del_s[2][BLK];
+  __shared__ __attribute__((aligned(16))) float tau_s[2][BLK];
+  __shared__ __attribute__((aligned(16))) float del_s[2][BLK];
 
   const int lane = lane_id(), w = wave_id();
   const int n = a.n, T = a.T;
@@ -101,7 +102,9 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
 
   // One 32-query half of the staged block against this wave's 32 keys:
   // S = Q K^T, dP = dO V^T (rows = queries), then dV += P^T dO, dK += dS^T Q.
-  auto block = [&](auto masked, const E* qt, const E* dt, const float* ts, const float* ds_,
+  // Masked sub-tiles set invalid scores to -inf first (the clamp of
+  // [x - tau]_+ then gives exactly 0), so one code path updates dK and dV.
+  auto block = [&](bool masked, const E* qt, const E* dt, const float* ts, const float* ds_,
                    int qh, int i0) {
     f32x16 s = zero16(), dp = zero16();
 #pragma unroll
@@ -109,18 +112,28 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
       s = M::mma(lds_row_frag<E, D>(qt, 32 * qh + (lane & 31), kk), kf[kk], s);
       dp = M::mma(lds_row_frag<E, D>(dt, 32 * qh + (lane & 31), kk), vf[kk], dp);
     }
+    if (masked) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = i0 + crow(r);
+        if (!(i < n && j < n && (!a.causal || j <= i))) s[r] = -INFINITY;
+      }
+    }
     float p[16], dsv[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int qi = 32 * qh + crow(r);
-      float zp = relu_z(c, s[r], ts[qi]);
-      if constexpr (decltype(masked)::value) {
-        const int i = i0 + crow(r);
-        zp = (i < n && j < n && (!a.causal || j <= i)) ? zp : 0.f;
+    for (int g4 = 0; g4 < 4; ++g4) {
+      // rows 8 g4 + 4h + (0..3) of this half: one 16-byte read each for tau, delta
+      const int q4 = 32 * qh + 8 * g4 + 4 * (lane >> 5);
+      const f32x4 tq = *reinterpret_cast<const f32x4*>(ts + q4);
+      const f32x4 dq4 = *reinterpret_cast<const f32x4*>(ds_ + q4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * g4 + e;
+        const float zp = relu_z(c, s[r], tq[e]);
+        float u;
+        Gamma<GK>::pu(zp, g, p[r], u);
+        dsv[r] = u * (dp[r] - dq4[e]);
       }
-      float u;
-      Gamma<GK>::pu(zp, g, p[r], u);
-      dsv[r] = u * (dp[r] - ds_[qi]);
     }
 #pragma unroll
     for (int t = 0; t < PS; ++t) {
@@ -165,10 +178,8 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
     for (int qh = 0; qh < 2; ++qh) {
       const int i0 = qb * BLK + 32 * qh;
       if (i0 >= n || (a.causal && k0 > i0 + 31)) continue;
-      if (i0 + 31 >= n || k0 + 31 >= n || (a.causal && k0 + 31 > i0))
-        block(std::true_type{}, qt, dt, tau_s[e & 1], del_s[e & 1], qh, i0);
-      else
-        block(std::false_type{}, qt, dt, tau_s[e & 1], del_s[e & 1], qh, i0);
+      const bool masked = i0 + 31 >= n || k0 + 31 >= n || (a.causal && k0 + 31 > i0);
+      block(masked, qt, dt, tau_s[e & 1], del_s[e & 1], qh, i0);
     }
   }
 
@@ -239,22 +250,26 @@ __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
     return 1;
   };
   // One 32-key half of the staged block: S^T = K Q^T, dP^T = V dO^T
-  // (rows = keys, columns = this wave's queries), then dQ += dS K.
-  auto block = [&](auto masked, const E* kt, const E* vt, int sub, int j0) {
+  // (rows = keys, columns = this wave's queries), then dQ += dS K.  Masked
+  // sub-tiles set invalid scores to -inf, so one code path updates dQ.
+  auto block = [&](bool masked, const E* kt, const E* vt, int sub, int j0) {
     f32x16 s = zero16(), dp = zero16();
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       s = M::mma(lds_row_frag<E, D>(kt, 32 * sub + (lane & 31), kk), qf[kk], s);
       dp = M::mma(lds_row_frag<E, D>(vt, 32 * sub + (lane & 31), kk), df[kk], dp);
     }
+    if (masked) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int jj = j0 + crow(r);
+        if (!(jj < n && (!a.causal || jj <= i))) s[r] = -INFINITY;
+      }
+    }
     float dsv[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      float zp = relu_z(c, s[r], tau);
-      if constexpr (decltype(masked)::value) {
-        const int jj = j0 + crow(r);
-        zp = (jj < n && (!a.causal || jj <= i)) ? zp : 0.f;
-      }
+      const float zp = relu_z(c, s[r], tau);
       float p, u;
       Gamma<GK>::pu(zp, g, p, u);
       dsv[r] = u * (dp[r] - del);
@@ -286,10 +301,8 @@ __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
     const E* vt = vbuf[e & 1];
     const int j0 = list[e] * BLK;
     const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
-    if (k0 == 1) block(std::false_type{}, kt, vt, 0, j0);
-    else if (k0 == 2) block(std::true_type{}, kt, vt, 0, j0);
-    if (k1 == 1) block(std::false_type{}, kt, vt, 1, j0 + 32);
-    else if (k1 == 2) block(std::true_type{}, kt, vt, 1, j0 + 32);
+    if (k0) block(k0 == 2, kt, vt, 0, j0);
+    if (k1) block(k1 == 2, kt, vt, 1, j0 + 32);
   }
 
   if (!wave_ok) return;

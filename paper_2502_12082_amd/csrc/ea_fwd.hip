@@ -110,15 +110,12 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
     return 1;
   };
   // P (and U) of one 32-key sub-tile, then O += P V (and U V into O2).
-  auto apply = [&](auto masked, const f32x16& s, const E* vt, int sub, int j0) {
+  // Masked sub-tiles arrive with invalid scores already set to -inf.
+  auto apply = [&](const f32x16& s, const E* vt, int sub) {
     float p[16], u[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      float zp = relu_z(c, s[r], tau);
-      if constexpr (decltype(masked)::value) {
-        const int j = j0 + crow(r);
-        zp = (j < n && (!a.causal || j <= i)) ? zp : 0.f;
-      }
+      const float zp = relu_z(c, s[r], tau);
       if constexpr (TRAIN) {
         Gamma<GK>::pu(zp, g, p[r], u[r]);
         usum += u[r];
@@ -140,6 +137,13 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
           if constexpr (!M::exact_operands) o2[nt] = M::mma(ul, vb, o2[nt]);
         }
       }
+    }
+  };
+  auto mask_tile = [&](f32x16& s, int j0) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = j0 + crow(r);
+      if (!(j < n && (!a.causal || j <= i))) s[r] = -INFINITY;
     }
   };
 
@@ -165,10 +169,10 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
       if (k0) s0 = M::mma(lds_row_frag<E, D>(kt, lane & 31, kk), qf[kk], s0);
       if (k1) s1 = M::mma(lds_row_frag<E, D>(kt, 32 + (lane & 31), kk), qf[kk], s1);
     }
-    if (k0 == 1) apply(std::false_type{}, s0, vt, 0, j0);
-    else if (k0 == 2) apply(std::true_type{}, s0, vt, 0, j0);
-    if (k1 == 1) apply(std::false_type{}, s1, vt, 1, j0 + 32);
-    else if (k1 == 2) apply(std::true_type{}, s1, vt, 1, j0 + 32);
+    if (k0 == 2) mask_tile(s0, j0);
+    if (k1 == 2) mask_tile(s1, j0 + 32);
+    if (k0) apply(s0, vt, 0);
+    if (k1) apply(s1, vt, 1);
   }
 
   if (!wave_ok) return;

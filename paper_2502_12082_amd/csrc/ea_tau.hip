@@ -116,13 +116,16 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
   // ---- pass 0: row maximum of the raw scores (scale > 0, so the maximum of
   // x = c s is c times the maximum of s)
   float smax = -INFINITY;
-  auto max_tile = [&](auto masked, const f32x16& s, int j0) {
+  // Invalid keys of a masked sub-tile become -inf: they cannot be the
+  // maximum, and the clamp of [x - tau]_+ turns them into exactly 0.
+  auto mask_tile = [&](f32x16& s, int j0) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float v = s[r];
-      if constexpr (decltype(masked)::value) v = valid(j0 + crow(r)) ? v : -INFINITY;
-      smax = fmaxf(smax, v);
-    }
+    for (int r = 0; r < 16; ++r)
+      if (!valid(j0 + crow(r))) s[r] = -INFINITY;
+  };
+  auto max_tile = [&](const f32x16& s) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) smax = fmaxf(smax, s[r]);
   };
   stream([&](int kb, const E* kt) {
     const int j0 = kb * BLK;
@@ -130,10 +133,10 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
     if (k0 == 0 && k1 == 0) return;
     f32x16 s0, s1;
     scores(kt, k0 != 0, k1 != 0, s0, s1);
-    if (k0 == 1) max_tile(std::false_type{}, s0, j0);
-    else if (k0 == 2) max_tile(std::true_type{}, s0, j0);
-    if (k1 == 1) max_tile(std::false_type{}, s1, j0 + 32);
-    else if (k1 == 2) max_tile(std::true_type{}, s1, j0 + 32);
+    if (k0 == 2) mask_tile(s0, j0);
+    if (k1 == 2) mask_tile(s1, j0 + 32);
+    if (k0) max_tile(s0);
+    if (k1) max_tile(s1);
   });
   smax = fmaxf(smax, __shfl_xor(smax, 32));
 
@@ -153,12 +156,11 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
     // count of the support is accumulated as sum ceil(z) (z is in [0, 1]).
     float m0 = 0.f, m1 = 0.f, m2 = 0.f;
     // Adds one sub-tile; returns whether it holds a positive probability.
-    auto eval_tile = [&](auto masked, const f32x16& s, int j0) {
+    auto eval_tile = [&](const f32x16& s) {
       float t0 = 0.f, t1 = 0.f, t2 = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float zp = relu_z(c, s[r], tau);
-        if constexpr (decltype(masked)::value) zp = valid(j0 + crow(r)) ? zp : 0.f;
+        const float zp = relu_z(c, s[r], tau);
         if constexpr (GK == 1) {
           t0 += zp;
           t1 += ceilf(zp);
@@ -192,11 +194,11 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
       if (k0 == 0 && k1 == 0) return;
       f32x16 s0, s1;
       scores(kt, k0 != 0, k1 != 0, s0, s1);
+      if (k0 == 2) mask_tile(s0, j0);
+      if (k1 == 2) mask_tile(s1, j0 + 32);
       bool any = false;
-      if (k0 == 1) any |= eval_tile(std::false_type{}, s0, j0);
-      else if (k0 == 2) any |= eval_tile(std::true_type{}, s0, j0);
-      if (k1 == 1) any |= eval_tile(std::false_type{}, s1, j0 + 32);
-      else if (k1 == 2) any |= eval_tile(std::true_type{}, s1, j0 + 32);
+      if (k0) any |= eval_tile(s0);
+      if (k1) any |= eval_tile(s1);
       const unsigned long long hit = __ballot(any);
       if (lane == 0) bits[w * MAX_KEY_BLOCKS + kb] = hit != 0ull;
     });
