@@ -151,10 +151,12 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
   };
 
   float tv = 0.f, dlv = 0.f;
+  DmaPlan<E, D, BWD_NT> dma;
+  dma.init();
   auto issue = [&](int e) {
     const int qb = list[e];
-    tile_dma<E, D, BWD_NT>(qbuf[e & 1], Qg, qb * BLK, n);
-    tile_dma<E, D, BWD_NT>(dobuf[e & 1], dOg, qb * BLK, n);
+    dma.issue(qbuf[e & 1], Qg, qb * BLK, n);
+    dma.issue(dobuf[e & 1], dOg, qb * BLK, n);
     if (threadIdx.x < BLK) {
       const int r = min(qb * BLK + (int)threadIdx.x, n - 1);
       tv = taug[r];
@@ -287,10 +289,12 @@ __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
     }
   };
 
+  DmaPlan<E, D, BWD_NT> dma;
+  dma.init();
   auto issue = [&](int e) {
     const int kb = list[e];
-    tile_dma<E, D, BWD_NT>(kbuf[e & 1], Kg, kb * BLK, n);
-    tile_dma<E, D, BWD_NT>(vbuf[e & 1], Vg, kb * BLK, n);
+    dma.issue(kbuf[e & 1], Kg, kb * BLK, n);
+    dma.issue(vbuf[e & 1], Vg, kb * BLK, n);
   };
   if (cnt > 0) issue(0);
   for (int e = 0; e < cnt; ++e) {

@@ -137,7 +137,7 @@ __device__ __forceinline__ typename Mma<E>::frag load_row_frag_global(const E* b
 //
 // A 64 x D tile of a [*, D] row-major global matrix is staged in LDS
 // row-major in 16-byte chunks, chunk (r, c) of tile row r stored at chunk
-// position r * CPR + (c ^ (r % CPR)) (CPR chunks per row).  The XOR swizzle
+// position r * CPR + (c ^ swz(r)) (CPR chunks per row).  The XOR pattern
 // spreads both access patterns over the banks: 32 lanes reading one chunk
 // column of 32 rows (MFMA row fragments), and the 8-row x 32-column blocks
 // read by the transposing loads.
@@ -155,7 +155,23 @@ struct Tile {
   static constexpr int CPR = D / VEC;              // chunks per row
   static constexpr int CHUNKS = BLK * CPR;
   static constexpr int ELEMS = BLK * D;
-  __device__ __forceinline__ static int chunk_pos(int r, int c) { return r * CPR + (c ^ (r & (CPR - 1))); }
+  // Chunk XOR pattern of tile row r, a bijection on the rows of each
+  // 16-row group (32 lanes reading one chunk column hit distinct banks);
+  // with 16 chunks per row the low two row bits also move whole 4-chunk
+  // groups, and with 8 chunks per row (two rows per 64 banks) row r and
+  // r + 2 differ in chunk bit 2, so the 4-row x 4-chunk blocks of a
+  // transposing read spread over all 64 banks.
+  __device__ __forceinline__ static int swz(int r) {
+    if constexpr (CPR == 16) {
+      return ((r & 3) << 2) | ((r >> 2) & 3);
+    } else if constexpr (CPR == 8) {
+      const int k = (r >> 1) & 7;
+      return ((k & 1) << 2) | (k >> 1);
+    } else {
+      return r & (CPR - 1);
+    }
+  }
+  __device__ __forceinline__ static int chunk_pos(int r, int c) { return r * CPR + (c ^ swz(r)); }
   // element offset of (row r, column col)
   __device__ __forceinline__ static int elem(int r, int col) {
     return chunk_pos(r, col / VEC) * VEC + (col & (VEC - 1));
@@ -171,27 +187,48 @@ __device__ __forceinline__ lds_void_t* to_lds(const void* p) {
 }
 
 // Asynchronous copy of tile rows [row0, row0 + 64) of g ([nrows, D]) into
-// `tile`, spread over the NT threads of the workgroup.
+// an LDS tile, spread over the NT threads of the workgroup.  The element
+// offset of every chunk this lane fetches is computed once (init); a copy
+// is then one uniform base plus those offsets, with the row clamp only on
+// the last, partial tile.
 template <typename E, int D, int NT>
-__device__ __forceinline__ void tile_dma(E* tile, const E* g, int row0, int nrows) {
+struct DmaPlan {
   using TL = Tile<E, D>;
-  constexpr int INSTR = TL::CHUNKS / 64;
-  constexpr int NW = NT / 64;
-  static_assert(INSTR % NW == 0, "tile instructions must divide the waves");
-#if defined(__HIP_DEVICE_COMPILE__)  // gfx950 builtin; kernels' lambdas are also parsed for the host
-  const int l = lane_id();
+  static constexpr int NW = NT / 64;
+  static constexpr int PER = TL::CHUNKS / 64 / NW;  // wave instructions per tile
+  static_assert(TL::CHUNKS % (64 * NW) == 0, "tile chunks must divide the waves");
+  int off[PER];
+
+  __device__ __forceinline__ void init() {
 #pragma unroll
-  for (int k0 = 0; k0 < INSTR; k0 += NW) {
-    const int k = k0 + wave_id();
-    const int p = 64 * k + l;
-    const int r = p / TL::CPR;
-    const int c = (p % TL::CPR) ^ (r & (TL::CPR - 1));
-    const int row = min(row0 + r, nrows - 1);
-    __builtin_amdgcn_global_load_lds(g + (size_t)row * D + c * TL::VEC, to_lds(tile + 64 * k * TL::VEC),
-                                     16, 0, 0);
+    for (int i = 0; i < PER; ++i) {
+      const int p = 64 * (i * NW + wave_id()) + lane_id();
+      const int r = p / TL::CPR;
+      off[i] = r * D + ((p % TL::CPR) ^ TL::swz(r)) * TL::VEC;
+    }
   }
+
+  __device__ __forceinline__ void issue(E* tile, const E* g, int row0, int nrows) const {
+#if defined(__HIP_DEVICE_COMPILE__)  // gfx950 builtin; kernels' lambdas are also parsed for the host
+    const E* base = g + (size_t)row0 * D;
+    if (row0 + BLK <= nrows) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i)
+        __builtin_amdgcn_global_load_lds(base + off[i], to_lds(tile + 64 * (i * NW + wave_id()) * TL::VEC),
+                                         16, 0, 0);
+    } else {
+      const int last = nrows - 1 - row0;  // rows past the end repeat the last row
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int r = off[i] / D;
+        const int o = off[i] + (min(r, last) - r) * D;
+        __builtin_amdgcn_global_load_lds(base + o, to_lds(tile + 64 * (i * NW + wave_id()) * TL::VEC),
+                                         16, 0, 0);
+      }
+    }
 #endif
-}
+  }
+};
 
 // Waits for this wave's outstanding global loads, global_load_lds included
 // (s_waitcnt vmcnt(0)); follow with a barrier before reading the tiles.

@@ -147,10 +147,12 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
     }
   };
 
+  DmaPlan<E, D, FWD_NT> dma;
+  dma.init();
   auto issue = [&](int e) {
     const int kb = list[e];
-    tile_dma<E, D, FWD_NT>(kbuf[e & 1], K, kb * BLK, n);
-    tile_dma<E, D, FWD_NT>(vbuf[e & 1], V, kb * BLK, n);
+    dma.issue(kbuf[e & 1], K, kb * BLK, n);
+    dma.issue(vbuf[e & 1], V, kb * BLK, n);
   };
   if (cnt > 0) issue(0);
   for (int e = 0; e < cnt; ++e) {
@@ -166,8 +168,8 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
     f32x16 s0 = zero16(), s1 = zero16();
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      if (k0) s0 = M::mma(lds_row_frag<E, D>(kt, lane & 31, kk), qf[kk], s0);
-      if (k1) s1 = M::mma(lds_row_frag<E, D>(kt, 32 + (lane & 31), kk), qf[kk], s1);
+      s0 = M::mma(lds_row_frag<E, D>(kt, lane & 31, kk), qf[kk], s0);
+      s1 = M::mma(lds_row_frag<E, D>(kt, 32 + (lane & 31), kk), qf[kk], s1);
     }
     if (k0 == 2) mask_tile(s0, j0);
     if (k1 == 2) mask_tile(s1, j0 + 32);

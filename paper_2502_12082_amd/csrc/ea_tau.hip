@@ -70,12 +70,14 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
 
   // Streams every key block the workgroup needs, double-buffered: block
   // kb + 1 is copied into LDS while `body(kb, tile)` works on block kb.
+  DmaPlan<E, D, TAU_NT> dma;
+  dma.init();
   auto stream = [&](auto&& body) {
-    tile_dma<E, D, TAU_NT>(kbuf[0], K, 0, n);
+    dma.issue(kbuf[0], K, 0, n);
     for (int kb = 0; kb < nkb; ++kb) {
       dma_wait();
       __syncthreads();
-      if (kb + 1 < nkb) tile_dma<E, D, TAU_NT>(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
+      if (kb + 1 < nkb) dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
       body(kb, kbuf[kb & 1]);
     }
     __syncthreads();  // the next pass refills buffer 0
@@ -83,25 +85,18 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
 
   // S^T sub-tiles of the staged block: keys [0, 32) and [32, 64) x this
   // wave's 32 queries; value r of lane l is key 32 sub + crow(r), query l%32.
-  // The two accumulation chains are interleaved so neither waits on the other.
-  auto scores = [&](const E* kt, bool need0, bool need1, f32x16& s0, f32x16& s1) {
+  // The two accumulation chains are interleaved so neither waits on the
+  // other; both are computed whenever the block has a valid key (a half with
+  // none is then simply not used).
+  auto scores = [&](const E* kt, f32x16& s0, f32x16& s1) {
     s0 = zero16();
     s1 = zero16();
-    if (need0 && need1) {
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        const typename M::frag a0 = lds_row_frag<E, D>(kt, (lane & 31), kk);
-        const typename M::frag a1 = lds_row_frag<E, D>(kt, 32 + (lane & 31), kk);
-        s0 = M::mma(a0, qf[kk], s0);
-        s1 = M::mma(a1, qf[kk], s1);
-      }
-    } else if (need0) {
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) s0 = M::mma(lds_row_frag<E, D>(kt, (lane & 31), kk), qf[kk], s0);
-    } else if (need1) {
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-        s1 = M::mma(lds_row_frag<E, D>(kt, 32 + (lane & 31), kk), qf[kk], s1);
+    for (int kk = 0; kk < KS; ++kk) {
+      const typename M::frag a0 = lds_row_frag<E, D>(kt, (lane & 31), kk);
+      const typename M::frag a1 = lds_row_frag<E, D>(kt, 32 + (lane & 31), kk);
+      s0 = M::mma(a0, qf[kk], s0);
+      s1 = M::mma(a1, qf[kk], s1);
     }
   };
   // Sub-tile state for the calling wave: 0 = nothing valid, 1 = all valid,
@@ -132,7 +127,7 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
     const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
     if (k0 == 0 && k1 == 0) return;
     f32x16 s0, s1;
-    scores(kt, k0 != 0, k1 != 0, s0, s1);
+    scores(kt, s0, s1);
     if (k0 == 2) mask_tile(s0, j0);
     if (k1 == 2) mask_tile(s1, j0 + 32);
     if (k0) max_tile(s0);
@@ -193,7 +188,7 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
       const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
       if (k0 == 0 && k1 == 0) return;
       f32x16 s0, s1;
-      scores(kt, k0 != 0, k1 != 0, s0, s1);
+      scores(kt, s0, s1);
       if (k0 == 2) mask_tile(s0, j0);
       if (k1 == 2) mask_tile(s1, j0 + 32);
       bool any = false;
