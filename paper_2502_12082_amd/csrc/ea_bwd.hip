@@ -204,8 +204,15 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
 
 // --------------------------------------------------------------------- dQ
 
+constexpr int DQ_NT = 256;
+
+// One 64-row query block per workgroup of 4 waves: wave w takes query half
+// qh = w % 2 and, of every listed key block, key half kh = w / 2, so each
+// wave holds only its 32 query rows and one partial dQ; the two key-half
+// partials are summed through LDS at the end.  Halving the per-wave state
+// lets two waves share each SIMD.
 template <typename E, int D, int GK>
-__global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
+__global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
   using TL = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
@@ -213,13 +220,15 @@ __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
   constexpr int PS = perm_steps<E>();
   __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
   __shared__ __attribute__((aligned(16))) E vbuf[2][TL::ELEMS];
+  static_assert(2 * NTD * 16 * 64 * sizeof(float) <= sizeof(kbuf), "dQ exchange must fit kbuf");
 
   const int lane = lane_id(), w = wave_id();
+  const int qh = w & 1, kh = w >> 1;
   const int n = a.n, T = a.T;
   const int bh = blockIdx.x % a.BH;
   int qb = blockIdx.x / a.BH;
   if (a.causal) qb = T - 1 - qb;  // longest lists first
-  const int q0 = qb * BLK + 32 * w;
+  const int q0 = qb * BLK + 32 * qh;
   const int i = q0 + (lane & 31);
   const bool wave_ok = q0 < n;
   const int wave_last = min(n - 1, q0 + 31);
@@ -246,22 +255,38 @@ __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
 #pragma unroll
   for (int t = 0; t < NTD; ++t) dq[t] = zero16();
 
+  // 0 = no valid key for this wave, 1 = all valid, 2 = per-element masking
   auto sub_kind = [&](int j0) {
     if (!wave_ok || j0 >= n || (a.causal && j0 > wave_last)) return 0;
     if (j0 + 31 >= n || (a.causal && j0 + 31 > q0)) return 2;
     return 1;
   };
-  // One 32-key half of the staged block: S^T = K Q^T, dP^T = V dO^T
-  // (rows = keys, columns = this wave's queries), then dQ += dS K.  Masked
-  // sub-tiles set invalid scores to -inf, so one code path updates dQ.
-  auto block = [&](bool masked, const E* kt, const E* vt, int sub, int j0) {
+
+  DmaPlan<E, D, DQ_NT> dma;
+  dma.init();
+  auto issue = [&](int e) {
+    const int kb = list[e];
+    dma.issue(kbuf[e & 1], Kg, kb * BLK, n);
+    dma.issue(vbuf[e & 1], Vg, kb * BLK, n);
+  };
+  if (cnt > 0) issue(0);
+  for (int e = 0; e < cnt; ++e) {
+    dma_wait();
+    __syncthreads();
+    if (e + 1 < cnt) issue(e + 1);
+    const E* kt = kbuf[e & 1];
+    const E* vt = vbuf[e & 1];
+    const int j0 = list[e] * BLK + 32 * kh;
+    const int kind = sub_kind(j0);
+    if (kind == 0) continue;
+    // S^T = K Q^T and dP^T = V dO^T for this wave's 32 keys x 32 queries
     f32x16 s = zero16(), dp = zero16();
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      s = M::mma(lds_row_frag<E, D>(kt, 32 * sub + (lane & 31), kk), qf[kk], s);
-      dp = M::mma(lds_row_frag<E, D>(vt, 32 * sub + (lane & 31), kk), df[kk], dp);
+      s = M::mma(lds_row_frag<E, D>(kt, 32 * kh + (lane & 31), kk), qf[kk], s);
+      dp = M::mma(lds_row_frag<E, D>(vt, 32 * kh + (lane & 31), kk), df[kk], dp);
     }
-    if (masked) {
+    if (kind == 2) {  // invalid keys -> -inf, so [x - tau]_+ is exactly 0 there
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int jj = j0 + crow(r);
@@ -282,41 +307,33 @@ __global__ __launch_bounds__(BWD_NT) void dq_kernel(BwdArgs a) {
       M::pack_split(dsv, t, dh, dl);
 #pragma unroll
       for (int nt = 0; nt < NTD; ++nt) {
-        const typename M::frag kb_ = lds_perm_frag<E, D>(kt, 32 * nt, 32 * sub, t);
+        const typename M::frag kb_ = lds_perm_frag<E, D>(kt, 32 * nt, 32 * kh, t);
         dq[nt] = M::mma(dh, kb_, dq[nt]);
         if constexpr (!M::exact_operands) dq[nt] = M::mma(dl, kb_, dq[nt]);
       }
     }
-  };
-
-  DmaPlan<E, D, BWD_NT> dma;
-  dma.init();
-  auto issue = [&](int e) {
-    const int kb = list[e];
-    dma.issue(kbuf[e & 1], Kg, kb * BLK, n);
-    dma.issue(vbuf[e & 1], Vg, kb * BLK, n);
-  };
-  if (cnt > 0) issue(0);
-  for (int e = 0; e < cnt; ++e) {
-    dma_wait();
-    __syncthreads();
-    if (e + 1 < cnt) issue(e + 1);
-    const E* kt = kbuf[e & 1];
-    const E* vt = vbuf[e & 1];
-    const int j0 = list[e] * BLK;
-    const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
-    if (k0) block(k0 == 2, kt, vt, 0, j0);
-    if (k1) block(k1 == 2, kt, vt, 1, j0 + 32);
   }
 
-  if (!wave_ok) return;
+  // sum the two key-half partials: kh = 1 hands its accumulators over in LDS
+  __syncthreads();
+  float* xch = reinterpret_cast<float*>(&kbuf[0][0]);
+  if (kh == 1) {
+#pragma unroll
+    for (int nt = 0; nt < NTD; ++nt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) xch[((qh * NTD + nt) * 16 + r) * 64 + lane] = dq[nt][r];
+  }
+  __syncthreads();
+  if (kh == 1 || !wave_ok) return;
   float* dQ = a.dq + head;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int ir = q0 + crow(r);
     if (ir < n) {
 #pragma unroll
-      for (int nt = 0; nt < NTD; ++nt) dQ[(size_t)ir * D + 32 * nt + (lane & 31)] = a.scale * dq[nt][r];
+      for (int nt = 0; nt < NTD; ++nt)
+        dQ[(size_t)ir * D + 32 * nt + (lane & 31)] =
+            a.scale * (dq[nt][r] + xch[((qh * NTD + nt) * 16 + r) * 64 + lane]);
     }
   }
 }
@@ -335,7 +352,7 @@ hipError_t launch_dkdv_d(const BwdArgs& a, hipStream_t s) {
 
 template <typename E, int D>
 hipError_t launch_dq_d(const BwdArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)(a.BH * a.T)), block(BWD_NT);
+  dim3 grid((unsigned)(a.BH * a.T)), block(DQ_NT);
   switch (a.gk) {
     case 1: hipLaunchKernelGGL((dq_kernel<E, D, 1>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((dq_kernel<E, D, 2>), grid, block, 0, s, a); break;
