@@ -23,6 +23,9 @@ ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
+    # fp32 d=128 variants cannot reach the two-waves-per-SIMD target the bf16
+    # ones are built for; the compiler reports that per instantiation
+    "-Wno-pass-failed",
     # no packed fp32 VALU instructions in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(ROOT, "include"),

@@ -60,10 +60,15 @@ __global__ __launch_bounds__(CMP_NT) void compact_kernel(CompactArgs a) {
 
 // --------------------------------------------------------------- forward
 
-constexpr int FWD_NT = 128;
+constexpr int FWD_NT = 256;
 
+// One 64-row query block per workgroup of 4 waves: wave w takes query half
+// qh = w % 2 and, of every listed key block, key half kh = w / 2.  Each wave
+// accumulates partial O (and U V, sum U) over its key halves; the two
+// partials of a query half are summed through LDS at the end.  The smaller
+// per-wave state lets two waves share each SIMD.
 template <typename E, int D, int GK, bool TRAIN>
-__global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
+__global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
   using TL = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
@@ -71,13 +76,16 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
   constexpr int PS = perm_steps<E>();
   __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
   __shared__ __attribute__((aligned(16))) E vbuf[2][TL::ELEMS];
+  __shared__ float usum_x[2][64];
+  static_assert(2 * NTD * 16 * 64 * sizeof(float) <= sizeof(kbuf), "partial exchange must fit kbuf");
 
   const int lane = lane_id(), w = wave_id();
+  const int qh = w & 1, kh = w >> 1;
   const int n = a.n, T = a.T;
   const int bh = blockIdx.x % a.BH;
   int qb = blockIdx.x / a.BH;
   if (a.causal) qb = T - 1 - qb;  // longest lists first
-  const int q0 = qb * BLK + 32 * w;
+  const int q0 = qb * BLK + 32 * qh;
   const int i = q0 + (lane & 31);
   const bool wave_ok = q0 < n;
   const int wave_last = min(n - 1, q0 + 31);
@@ -99,7 +107,7 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
 #pragma unroll
   for (int t = 0; t < NTD; ++t) {
     o[t] = zero16();
-    o2[t] = zero16();
+    if constexpr (TRAIN) o2[t] = zero16();
   }
   float usum = 0.f;
 
@@ -109,9 +117,35 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
     if (j0 + 31 >= n || (a.causal && j0 + 31 > q0)) return 2;
     return 1;
   };
-  // P (and U) of one 32-key sub-tile, then O += P V (and U V into O2).
-  // Masked sub-tiles arrive with invalid scores already set to -inf.
-  auto apply = [&](const f32x16& s, const E* vt, int sub) {
+
+  DmaPlan<E, D, FWD_NT> dma;
+  dma.init();
+  auto issue = [&](int e) {
+    const int kb = list[e];
+    dma.issue(kbuf[e & 1], K, kb * BLK, n);
+    dma.issue(vbuf[e & 1], V, kb * BLK, n);
+  };
+  if (cnt > 0) issue(0);
+  for (int e = 0; e < cnt; ++e) {
+    dma_wait();
+    __syncthreads();
+    if (e + 1 < cnt) issue(e + 1);
+    const E* kt = kbuf[e & 1];
+    const E* vt = vbuf[e & 1];
+    const int j0 = list[e] * BLK + 32 * kh;
+    const int kind = sub_kind(j0);
+    if (kind == 0) continue;
+    // S^T = K Q^T for this wave's 32 keys x 32 queries
+    f32x16 s = zero16();
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) s = M::mma(lds_row_frag<E, D>(kt, 32 * kh + (lane & 31), kk), qf[kk], s);
+    if (kind == 2) {  // invalid keys -> -inf, so [x - tau]_+ is exactly 0 there
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = j0 + crow(r);
+        if (!(j < n && (!a.causal || j <= i))) s[r] = -INFINITY;
+      }
+    }
     float p[16], u[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -130,7 +164,7 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
       if constexpr (TRAIN) M::pack_split(u, t, uh, ul);
 #pragma unroll
       for (int nt = 0; nt < NTD; ++nt) {
-        const typename M::frag vb = lds_perm_frag<E, D>(vt, 32 * nt, 32 * sub, t);
+        const typename M::frag vb = lds_perm_frag<E, D>(vt, 32 * nt, 32 * kh, t);
         o[nt] = M::mma(pa, vb, o[nt]);
         if constexpr (TRAIN) {
           o2[nt] = M::mma(uh, vb, o2[nt]);
@@ -138,47 +172,47 @@ __global__ __launch_bounds__(FWD_NT) void fwd_kernel(FwdArgs a) {
         }
       }
     }
-  };
-  auto mask_tile = [&](f32x16& s, int j0) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int j = j0 + crow(r);
-      if (!(j < n && (!a.causal || j <= i))) s[r] = -INFINITY;
-    }
-  };
-
-  DmaPlan<E, D, FWD_NT> dma;
-  dma.init();
-  auto issue = [&](int e) {
-    const int kb = list[e];
-    dma.issue(kbuf[e & 1], K, kb * BLK, n);
-    dma.issue(vbuf[e & 1], V, kb * BLK, n);
-  };
-  if (cnt > 0) issue(0);
-  for (int e = 0; e < cnt; ++e) {
-    dma_wait();
-    __syncthreads();
-    if (e + 1 < cnt) issue(e + 1);
-    const E* kt = kbuf[e & 1];
-    const E* vt = vbuf[e & 1];
-    const int j0 = list[e] * BLK;
-    const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
-    if (k0 == 0 && k1 == 0) continue;
-    // S^T = K Q^T for both 32-key halves, two interleaved MFMA chains
-    f32x16 s0 = zero16(), s1 = zero16();
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      s0 = M::mma(lds_row_frag<E, D>(kt, lane & 31, kk), qf[kk], s0);
-      s1 = M::mma(lds_row_frag<E, D>(kt, 32 + (lane & 31), kk), qf[kk], s1);
-    }
-    if (k0 == 2) mask_tile(s0, j0);
-    if (k1 == 2) mask_tile(s1, j0 + 32);
-    if (k0) apply(s0, vt, 0);
-    if (k1) apply(s1, vt, 1);
   }
 
-  if (!wave_ok) return;
+  // Sum the two key-half partials of each query half through LDS: first O
+  // and sum U, then O2; kh = 1 hands over, kh = 0 adds and writes.
   if constexpr (TRAIN) usum += __shfl_xor(usum, 32);
+  float* xch = reinterpret_cast<float*>(&kbuf[0][0]);
+  auto xidx = [&](int nt, int r) { return ((qh * NTD + nt) * 16 + r) * 64 + lane; };
+  __syncthreads();
+  if (kh == 1) {
+#pragma unroll
+    for (int nt = 0; nt < NTD; ++nt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) xch[xidx(nt, r)] = o[nt][r];
+    if (lane < 32) usum_x[qh][lane] = usum;
+  }
+  __syncthreads();
+  if (kh == 0) {
+#pragma unroll
+    for (int nt = 0; nt < NTD; ++nt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[nt][r] += xch[xidx(nt, r)];
+    if constexpr (TRAIN) usum += usum_x[qh][lane & 31];
+  }
+  if constexpr (TRAIN) {
+    __syncthreads();
+    if (kh == 1) {
+#pragma unroll
+      for (int nt = 0; nt < NTD; ++nt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) xch[xidx(nt, r)] = o2[nt][r];
+    }
+    __syncthreads();
+    if (kh == 0) {
+#pragma unroll
+      for (int nt = 0; nt < NTD; ++nt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o2[nt][r] += xch[xidx(nt, r)];
+    }
+  }
+  if (kh == 1 || !wave_ok) return;
+
   E* O = static_cast<E*>(a.o) + head;
   float* O2 = a.o2 + head;
 #pragma unroll
