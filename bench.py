@@ -137,17 +137,10 @@ class Runner:
         else:
             n_valid = BH * T * T
         n_act = int(self.res.q_count.sum().item())
-        stats = self.res.stats.cpu().numpy().astype(np.int64)
-        nqt = (n + 127) // 128
-        # valid 64x64 blocks each 128-row solver workgroup streams
-        per_wg = np.empty(nqt, dtype=np.int64)
-        for qt in range(nqt):
-            rows = min(2, T - 2 * qt)
-            if self.params.causal:
-                per_wg[qt] = sum(min(T, 2 * qt + r + 1) for r in range(rows))
-            else:
-                per_wg[qt] = rows * T
-        solver_blocks = float((stats.reshape(BH, nqt) * per_wg[None, :]).sum())
+        stats = self.res.stats.cpu().numpy().astype(np.int64).reshape(BH, T)
+        # valid 64x64 blocks each query block streams per solver pass
+        per_qb = np.arange(1, T + 1) if self.params.causal else np.full(T, T)
+        solver_blocks = float((stats * per_qb[None, :]).sum())
         flops = {"tau_solve": solver_blocks * f_blk, "compact": 0.0, "bwd_delta": 0.0}
         for k_, m in PRODUCTS_PER_ACTIVE.items():
             flops[k_] = m * n_act * f_blk

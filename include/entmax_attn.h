@@ -70,8 +70,8 @@ typedef struct {
  *   q_index    i32   [BH, T, T]    row (b,h,i): Q_i ascending in its first q_count entries
  *   k_count    i32   [BH, T]       |K_j|, query blocks listed for key block j
  *   k_index    i32   [BH, T, T]    row (b,h,j): K_j ascending in its first k_count entries
- *   stats      i32   [BH, ceil(n/128)] optional (may be NULL): K passes run by each
- *                                  128-row solver workgroup (1 max pass + evaluations)
+ *   stats      i32   [BH, T]       optional (may be NULL): K passes the solver ran for each
+ *                                  64-row query block (1 max pass + evaluation passes)
  */
 typedef struct {
   float* tau;
@@ -147,6 +147,11 @@ ea_status entmax_attn_bwd_stage(int stage, const ea_shape* shape, const ea_param
 
 /* Static, human-readable name of a status code. */
 const char* entmax_attn_status_string(ea_status s);
+
+/* Name of the HIP error (e.g. "hipErrorInvalidConfiguration") behind the calling
+ * thread's most recent EA_ERR_HIP, or "" if that thread has seen none. Static
+ * storage; the caller does not free it. */
+const char* entmax_attn_last_hip_error(void);
 
 #ifdef __cplusplus
 }

@@ -21,13 +21,19 @@ if not os.path.exists(LIB_PATH):
     raise ImportError("libentmax_attn.so is not built; run `python paper_2502_12082_amd/build.py` "
                       "(or __graft_entry__.build()) first")
 
+# torch ships its own HIP and HSA runtimes.  Importing it first lets the
+# library's libamdhip64.so.7 dependency resolve to the copy torch already
+# loaded; loaded the other way round the process holds two runtimes, and
+# launches through the second one find no device.
+import torch  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 EA_OK, EA_ERR_INVALID_ARG, EA_ERR_UNSUPPORTED, EA_ERR_WORKSPACE, EA_ERR_HIP = range(5)
 EA_BF16, EA_F32 = 0, 1
 SYMBOLS = ("entmax_attn_default_params", "entmax_attn_sizes", "entmax_attn_fwd",
            "entmax_attn_bwd", "entmax_attn_fwd_stage", "entmax_attn_bwd_stage",
-           "entmax_attn_status_string")
+           "entmax_attn_status_string", "entmax_attn_last_hip_error")
 
 
 class Shape(ctypes.Structure):
@@ -73,13 +79,18 @@ _lib.entmax_attn_bwd_stage.argtypes = [ctypes.c_int, _P(Shape), _P(Params), _v, 
 _lib.entmax_attn_bwd_stage.restype = ctypes.c_int
 _lib.entmax_attn_status_string.argtypes = [ctypes.c_int]
 _lib.entmax_attn_status_string.restype = ctypes.c_char_p
+_lib.entmax_attn_last_hip_error.argtypes = []
+_lib.entmax_attn_last_hip_error.restype = ctypes.c_char_p
 
 
 class EntmaxAttnError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
-        super().__init__("%s: %s (status %d)" % (
-            where, _lib.entmax_attn_status_string(status).decode(), status))
+        msg = "%s: %s (status %d)" % (
+            where, _lib.entmax_attn_status_string(status).decode(), status)
+        if status == EA_ERR_HIP:
+            msg += ": " + _lib.entmax_attn_last_hip_error().decode()
+        super().__init__(msg)
 
 
 def _check(status: int, where: str):
@@ -128,13 +139,7 @@ def entmax_attn_bwd_stage(stage, shape, params, q, k, v, dout, res: ResidualPtrs
 
 # ------------------------------------------------------ torch conveniences
 
-def _torch():
-    import torch
-    return torch
-
-
 def make_shape(q) -> Shape:
-    torch = _torch()
     if q.dim() != 4:
         raise ValueError("expected [batch, heads, seqlen, head_dim]")
     if q.dtype == torch.bfloat16:
@@ -166,7 +171,6 @@ class Residuals:
     reads, sized by entmax_attn_sizes."""
 
     def __init__(self, shape: Shape, params: Params, device, with_stats: bool = True):
-        torch = _torch()
         z = entmax_attn_sizes(shape, params)
         BH, n, d = shape.batch * shape.heads, shape.seqlen, shape.head_dim
         T = (n + 63) // 64
@@ -189,13 +193,12 @@ class Residuals:
 
 
 def _stream_handle(device):
-    return _torch().cuda.current_stream(device).cuda_stream
+    return torch.cuda.current_stream(device).cuda_stream
 
 
 def forward(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_iter=None,
             tol=None, out=None, res: Residuals | None = None):
     """O and the residuals for Q, K, V ([B, H, n, d] bf16/fp32 CUDA tensors)."""
-    torch = _torch()
     for t in (q, k, v):
         if not t.is_cuda or not t.is_contiguous() or t.shape != q.shape or t.dtype != q.dtype:
             raise ValueError("q, k, v must be contiguous device tensors of one shape and dtype")
@@ -215,7 +218,6 @@ def forward(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_ite
 
 def backward(q, k, v, dout, res: Residuals, dq=None, dk=None, dv=None, workspace=None):
     """(dQ, dK, dV) in fp32 for the loss sum(dO * O) of the forward that filled res."""
-    torch = _torch()
     shape = make_shape(q)
     if dout.shape != q.shape or dout.dtype != q.dtype or not dout.is_contiguous():
         raise ValueError("dout must match q")

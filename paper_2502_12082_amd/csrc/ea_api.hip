@@ -65,7 +65,7 @@ void fill_sizes(const Dims& d, ea_sizes* z) {
   z->q_index = (size_t)(d.BH * d.T * d.T) * 4;
   z->k_count = z->q_count;
   z->k_index = z->q_index;
-  z->stats = (size_t)(d.BH * ((d.n + 127) / 128)) * 4;
+  z->stats = (size_t)(d.BH * d.T) * 4;
   z->ws_fwd = 0;
   z->ws_bwd = (size_t)(d.BH * d.n) * 4;
 }
@@ -82,7 +82,14 @@ ea_status check_tables(const ea_residuals* r) {
   return EA_OK;
 }
 
-ea_status from_hip(hipError_t e) { return e == hipSuccess ? EA_OK : EA_ERR_HIP; }
+// HIP error behind the calling thread's most recent EA_ERR_HIP.
+thread_local hipError_t last_hip_error = hipSuccess;
+
+ea_status from_hip(hipError_t e) {
+  if (e == hipSuccess) return EA_OK;
+  last_hip_error = e;
+  return EA_ERR_HIP;
+}
 
 }  // namespace
 }  // namespace ea
@@ -239,6 +246,10 @@ const char* entmax_attn_status_string(ea_status s) {
     case EA_ERR_HIP: return "HIP launch failure";
   }
   return "unknown status";
+}
+
+const char* entmax_attn_last_hip_error(void) {
+  return last_hip_error == hipSuccess ? "" : hipGetErrorName(last_hip_error);
 }
 
 }  // extern "C"

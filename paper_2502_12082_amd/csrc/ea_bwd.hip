@@ -341,32 +341,27 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
 template <typename E, int D>
 hipError_t launch_dkdv_d(const BwdArgs& a, hipStream_t s) {
   dim3 grid((unsigned)(a.BH * a.T)), block(BWD_NT);
-  switch (a.gk) {
-    case 1: hipLaunchKernelGGL((dkdv_kernel<E, D, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((dkdv_kernel<E, D, 2>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((dkdv_kernel<E, D, 4>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((dkdv_kernel<E, D, 0>), grid, block, 0, s, a); break;
-  }
-  return hipGetLastError();
+  auto kernel = dkdv_kernel<E, D, 0>;
+  if (a.gk == 1) kernel = dkdv_kernel<E, D, 1>;
+  if (a.gk == 2) kernel = dkdv_kernel<E, D, 2>;
+  if (a.gk == 4) kernel = dkdv_kernel<E, D, 4>;
+  return launch_kernel(kernel, grid, block, s, a);
 }
 
 template <typename E, int D>
 hipError_t launch_dq_d(const BwdArgs& a, hipStream_t s) {
   dim3 grid((unsigned)(a.BH * a.T)), block(DQ_NT);
-  switch (a.gk) {
-    case 1: hipLaunchKernelGGL((dq_kernel<E, D, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((dq_kernel<E, D, 2>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((dq_kernel<E, D, 4>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((dq_kernel<E, D, 0>), grid, block, 0, s, a); break;
-  }
-  return hipGetLastError();
+  auto kernel = dq_kernel<E, D, 0>;
+  if (a.gk == 1) kernel = dq_kernel<E, D, 1>;
+  if (a.gk == 2) kernel = dq_kernel<E, D, 2>;
+  if (a.gk == 4) kernel = dq_kernel<E, D, 4>;
+  return launch_kernel(kernel, grid, block, s, a);
 }
 
 template <typename E, int D>
 hipError_t launch_delta_d(const DeltaArgs& a, hipStream_t s) {
   dim3 grid((unsigned)((a.rows + 15) / 16)), block(256);
-  hipLaunchKernelGGL((delta_kernel<E, D>), grid, block, 0, s, a);
-  return hipGetLastError();
+  return launch_kernel(delta_kernel<E, D>, grid, block, s, a);
 }
 
 }  // namespace

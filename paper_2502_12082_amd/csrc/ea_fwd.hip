@@ -235,13 +235,11 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
 template <typename E, int D, bool TRAIN>
 hipError_t launch_fwd_dt(const FwdArgs& a, hipStream_t s) {
   dim3 grid((unsigned)(a.BH * a.T)), block(FWD_NT);
-  switch (a.gk) {
-    case 1: hipLaunchKernelGGL((fwd_kernel<E, D, 1, TRAIN>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((fwd_kernel<E, D, 2, TRAIN>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((fwd_kernel<E, D, 4, TRAIN>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((fwd_kernel<E, D, 0, TRAIN>), grid, block, 0, s, a); break;
-  }
-  return hipGetLastError();
+  auto kernel = fwd_kernel<E, D, 0, TRAIN>;
+  if (a.gk == 1) kernel = fwd_kernel<E, D, 1, TRAIN>;
+  if (a.gk == 2) kernel = fwd_kernel<E, D, 2, TRAIN>;
+  if (a.gk == 4) kernel = fwd_kernel<E, D, 4, TRAIN>;
+  return launch_kernel(kernel, grid, block, s, a);
 }
 
 template <typename E, int D>
@@ -254,8 +252,7 @@ hipError_t launch_fwd_d(const FwdArgs& a, bool train, hipStream_t s) {
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s) {
   const long long waves = 2LL * a.BH * a.T;
   dim3 grid((unsigned)((waves + CMP_NT / 64 - 1) / (CMP_NT / 64))), block(CMP_NT);
-  hipLaunchKernelGGL(compact_kernel, grid, block, 0, s, a);
-  return hipGetLastError();
+  return launch_kernel(compact_kernel, grid, block, s, a);
 }
 
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int head_dim, bool train, hipStream_t s) {

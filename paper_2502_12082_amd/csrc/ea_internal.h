@@ -21,7 +21,7 @@ struct TauArgs {
   const void* k;
   float* tau;         // [BH, n]
   uint8_t* mask;      // [BH, T, T]
-  int32_t* stats;     // [BH, ceil(n/128)] passes per workgroup, or null
+  int32_t* stats;     // [BH, T] K passes run for each 64-row query block, or null
   int BH, n, T;
   float c;            // (alpha - 1) * scale
   float alpha, gamma;
@@ -78,6 +78,14 @@ struct DeltaArgs {
 
 // Each launcher picks the instantiation for (dtype: 0 bf16 / 1 fp32, head_dim,
 // gamma kind) and returns the launch status.
+// Launches `kernel` with its one argument struct and returns the launch's own
+// status (not an error left behind by earlier HIP calls on this thread).
+template <typename A>
+inline hipError_t launch_kernel(void (*kernel)(A), dim3 grid, dim3 block, hipStream_t s, A a) {
+  void* args[] = {&a};
+  return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, args, 0, s);
+}
+
 hipError_t launch_tau(const TauArgs& a, int dtype, int head_dim, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int head_dim, bool train, hipStream_t s);

@@ -237,28 +237,27 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
 
   if (row_ok && lane < 32) a.tau[(size_t)bh * n + i] = tau;
   __syncthreads();
-  for (int x = threadIdx.x; x < 2 * T; x += TAU_NT) {
+  constexpr int QBLOCKS = TAU_WAVES / 2;  // 64-row mask rows per workgroup
+  for (int x = threadIdx.x; x < QBLOCKS * T; x += TAU_NT) {
     const int half = x / T, kb = x % T;
-    const int qb = 2 * qt + half;
+    const int qb = QBLOCKS * qt + half;
     if (qb < T) {
       const uint8_t b = bits[(2 * half) * MAX_KEY_BLOCKS + kb] | bits[(2 * half + 1) * MAX_KEY_BLOCKS + kb];
       a.mask[((size_t)bh * T + qb) * T + kb] = b;
+      if (a.stats && kb == 0) a.stats[(size_t)bh * T + qb] = passes;
     }
   }
-  if (a.stats && threadIdx.x == 0) a.stats[(size_t)bh * nqt + qt] = passes;
 }
 
 template <typename E, int D>
 hipError_t launch_tau_d(const TauArgs& a, hipStream_t s) {
   const int nqt = (a.n + TAU_ROWS - 1) / TAU_ROWS;
   dim3 grid((unsigned)(a.BH * nqt)), block(TAU_NT);
-  switch (a.gk) {
-    case 1: hipLaunchKernelGGL((tau_solve_kernel<E, D, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((tau_solve_kernel<E, D, 2>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((tau_solve_kernel<E, D, 4>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((tau_solve_kernel<E, D, 0>), grid, block, 0, s, a); break;
-  }
-  return hipGetLastError();
+  auto kernel = tau_solve_kernel<E, D, 0>;
+  if (a.gk == 1) kernel = tau_solve_kernel<E, D, 1>;
+  if (a.gk == 2) kernel = tau_solve_kernel<E, D, 2>;
+  if (a.gk == 4) kernel = tau_solve_kernel<E, D, 4>;
+  return launch_kernel(kernel, grid, block, s, a);
 }
 
 }  // namespace
