@@ -176,6 +176,36 @@ struct Tile {
   __device__ __forceinline__ static int elem(int r, int col) {
     return chunk_pos(r, col / VEC) * VEC + (col & (VEC - 1));
   }
+  // global element offset (within the 64-row block) of the chunk stored at
+  // chunk position p
+  __device__ __forceinline__ static int src_off(int p) {
+    const int r = p / CPR;
+    return r * D + ((p % CPR) ^ swz(r)) * VEC;
+  }
+};
+
+// A 64 x D tile read only as MFMA row fragments, stored row-major with one
+// 16-byte pad chunk after every row (row stride CPR + 1 chunks).  The 16
+// rows read by 16 consecutive lanes then start in 16 distinct 16-byte bank
+// groups (CPR + 1 is odd), so row-fragment reads are conflict-free, and the
+// chunk offset of k step kk is the same constant for every lane: the reads
+// of one row use one base address plus immediate offsets.  The pad chunks
+// are filled with a copy of the row's first chunk and never read.
+template <typename E, int D>
+struct PadTile {
+  static constexpr int VEC = 16 / (int)sizeof(E);
+  static constexpr int CPR = D / VEC;
+  static constexpr int RS = CPR + 1;  // row stride in chunks
+  static constexpr int CHUNKS = BLK * RS;
+  static constexpr int ELEMS = CHUNKS * VEC;
+  __device__ __forceinline__ static int chunk_pos(int r, int c) { return r * RS + c; }
+  __device__ __forceinline__ static int elem(int r, int col) {
+    return chunk_pos(r, col / VEC) * VEC + (col & (VEC - 1));
+  }
+  __device__ __forceinline__ static int src_off(int p) {
+    const int r = p / RS, c = p % RS;
+    return r * D + (c == CPR ? 0 : c) * VEC;
+  }
 };
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -187,48 +217,52 @@ __device__ __forceinline__ lds_void_t* to_lds(const void* p) {
 }
 
 // Asynchronous copy of tile rows [row0, row0 + 64) of g ([nrows, D]) into
-// an LDS tile, spread over the NT threads of the workgroup.  The element
-// offset of every chunk this lane fetches is computed once (init); a copy
-// is then one uniform base plus those offsets, with the row clamp only on
-// the last, partial tile.
-template <typename E, int D, int NT>
-struct DmaPlan {
-  using TL = Tile<E, D>;
+// an LDS tile of layout TL, spread over the NT threads of the workgroup:
+// wave instruction k (k = i * NW + wave) fills chunk positions
+// [64k, 64k + 64).  The element offset of every chunk this lane fetches is
+// computed once (init); a copy is then one uniform base plus those offsets,
+// with the row clamp only on the last, partial tile.
+template <typename TL, int D, int NT>
+struct TileDma {
   static constexpr int NW = NT / 64;
-  static constexpr int PER = TL::CHUNKS / 64 / NW;  // wave instructions per tile
-  static_assert(TL::CHUNKS % (64 * NW) == 0, "tile chunks must divide the waves");
+  static constexpr int NI = TL::CHUNKS / 64;        // wave instructions per tile
+  static constexpr int PER = (NI + NW - 1) / NW;    // per wave (the last may be idle)
+  static_assert(TL::CHUNKS % 64 == 0, "tile chunks must fill whole wave instructions");
   int off[PER];
 
   __device__ __forceinline__ void init() {
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int p = 64 * (i * NW + wave_id()) + lane_id();
-      const int r = p / TL::CPR;
-      off[i] = r * D + ((p % TL::CPR) ^ TL::swz(r)) * TL::VEC;
-    }
+    for (int i = 0; i < PER; ++i) off[i] = TL::src_off(64 * min(i * NW + wave_id(), NI - 1) + lane_id());
   }
 
+  template <typename E>
   __device__ __forceinline__ void issue(E* tile, const E* g, int row0, int nrows) const {
 #if defined(__HIP_DEVICE_COMPILE__)  // gfx950 builtin; kernels' lambdas are also parsed for the host
     const E* base = g + (size_t)row0 * D;
     if (row0 + BLK <= nrows) {
 #pragma unroll
-      for (int i = 0; i < PER; ++i)
-        __builtin_amdgcn_global_load_lds(base + off[i], to_lds(tile + 64 * (i * NW + wave_id()) * TL::VEC),
-                                         16, 0, 0);
+      for (int i = 0; i < PER; ++i) {
+        const int k = i * NW + wave_id();
+        if (NI % NW != 0 && k >= NI) break;
+        __builtin_amdgcn_global_load_lds(base + off[i], to_lds(tile + 64 * k * TL::VEC), 16, 0, 0);
+      }
     } else {
       const int last = nrows - 1 - row0;  // rows past the end repeat the last row
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
+        const int k = i * NW + wave_id();
+        if (NI % NW != 0 && k >= NI) break;
         const int r = off[i] / D;
         const int o = off[i] + (min(r, last) - r) * D;
-        __builtin_amdgcn_global_load_lds(base + o, to_lds(tile + 64 * (i * NW + wave_id()) * TL::VEC),
-                                         16, 0, 0);
+        __builtin_amdgcn_global_load_lds(base + o, to_lds(tile + 64 * k * TL::VEC), 16, 0, 0);
       }
     }
 #endif
   }
 };
+
+template <typename E, int D, int NT>
+using DmaPlan = TileDma<Tile<E, D>, D, NT>;
 
 // Waits for this wave's outstanding global loads, global_load_lds included
 // (s_waitcnt vmcnt(0)); follow with a barrier before reading the tiles.
@@ -238,6 +272,18 @@ __device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0x0F70);
 template <typename E, int D>
 __device__ __forceinline__ typename Mma<E>::frag lds_row_frag(const E* tile, int r, int kk) {
   using TL = Tile<E, D>;
+  const int h = lane_id() >> 5;
+  if constexpr (Mma<E>::EPL == 8) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(tile + TL::chunk_pos(r, 2 * kk + h) * 8));
+  } else {
+    return tile[TL::elem(r, 2 * kk + h)];
+  }
+}
+
+// A-operand row fragment of row r, k step kk, of a PadTile.
+template <typename E, int D>
+__device__ __forceinline__ typename Mma<E>::frag lds_row_frag_pad(const E* tile, int r, int kk) {
+  using TL = PadTile<E, D>;
   const int h = lane_id() >> 5;
   if constexpr (Mma<E>::EPL == 8) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(tile + TL::chunk_pos(r, 2 * kk + h) * 8));
@@ -279,6 +325,18 @@ __device__ __forceinline__ typename Mma<E>::frag lds_perm_frag(const E* tile, in
 // [z]_+ and folds into one v_fma_f32 with the clamp bit.
 __device__ __forceinline__ float relu_z(float c, float s, float tau) {
   return __builtin_amdgcn_fmed3f(fmaf(c, s, -tau), 0.f, 1.f);
+}
+
+// 1 if zp > 0, else 0, for zp from the clamp above (+0, -0 or positive; -0
+// has the sign bit set and reads as a negative integer): one v_med3_i32.
+__device__ __forceinline__ int in_support(float zp) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  int r;
+  asm("v_med3_i32 %0, %1, 0, 1" : "=v"(r) : "v"(zp));
+  return r;
+#else
+  return zp > 0.f ? 1 : 0;
+#endif
 }
 
 // GK = gamma for the integer cases 1 (alpha = 2), 2 (alpha = 1.5),

@@ -34,12 +34,15 @@ constexpr int TAU_NT = 64 * TAU_WAVES;
 constexpr int TAU_ROWS = 32 * TAU_WAVES;
 
 template <typename E, int D, int GK>
-__global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
-  using TL = Tile<E, D>;
+__global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
+  using TL = PadTile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
+  constexpr int BW = MAX_KEY_BLOCKS / 32;  // mask words per wave
   __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
-  __shared__ uint8_t bits[TAU_WAVES * MAX_KEY_BLOCKS];
+  // bit kb of word kb / 32: key block kb holds a positive probability for
+  // one of the wave's 32 rows (written by the wave's lane 0 only)
+  __shared__ uint32_t bits[TAU_WAVES * BW];
 
   const int lane = lane_id(), w = wave_id();
   const int n = a.n, T = a.T;
@@ -63,14 +66,14 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) qf[kk] = load_row_frag_global<E, D>(Q, i, n, kk);
 
-  for (int x = threadIdx.x; x < TAU_WAVES * T; x += TAU_NT)
-    bits[(x / T) * MAX_KEY_BLOCKS + (x % T)] = 0;
+  const int TW = (T + 31) / 32;
+  for (int x = threadIdx.x; x < TAU_WAVES * TW; x += TAU_NT) bits[(x / TW) * BW + (x % TW)] = 0;
 
   const float c = a.c;
 
   // Streams every key block the workgroup needs, double-buffered: block
   // kb + 1 is copied into LDS while `body(kb, tile)` works on block kb.
-  DmaPlan<E, D, TAU_NT> dma;
+  TileDma<TL, D, TAU_NT> dma;
   dma.init();
   auto stream = [&](auto&& body) {
     dma.issue(kbuf[0], K, 0, n);
@@ -93,8 +96,8 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
     s1 = zero16();
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      const typename M::frag a0 = lds_row_frag<E, D>(kt, (lane & 31), kk);
-      const typename M::frag a1 = lds_row_frag<E, D>(kt, 32 + (lane & 31), kk);
+      const typename M::frag a0 = lds_row_frag_pad<E, D>(kt, (lane & 31), kk);
+      const typename M::frag a1 = lds_row_frag_pad<E, D>(kt, 32 + (lane & 31), kk);
       s0 = M::mma(a0, qf[kk], s0);
       s1 = M::mma(a1, qf[kk], s1);
     }
@@ -120,7 +123,7 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
   };
   auto max_tile = [&](const f32x16& s) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) smax = fmaxf(smax, s[r]);
+    for (int r = 0; r < 16; r += 2) smax = fmaxf(smax, fmaxf(s[r], s[r + 1]));
   };
   stream([&](int kb, const E* kt) {
     const int j0 = kb * BLK;
@@ -146,58 +149,77 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
   const float g = a.gamma;
   int passes = 1;
   for (int it = 0;; ++it) {
-    // ---- evaluation pass at tau: s0 = sum z^gamma, s1 = sum z^(gamma-1),
-    // s2 = sum z^(gamma-2) over the strict support z > 0; for gamma = 1, 2 the
-    // count of the support is accumulated as sum ceil(z) (z is in [0, 1]).
+    // ---- evaluation pass at tau: m0 = sum z^gamma, m1 = sum z^(gamma-1),
+    // m2 = sum z^(gamma-2) over the strict support z > 0.  For gamma = 1, 2
+    // the last of these is the size of the support, counted exactly as an
+    // integer (mc).
     float m0 = 0.f, m1 = 0.f, m2 = 0.f;
+    int mc = 0;
     // Adds one sub-tile; returns whether it holds a positive probability.
     auto eval_tile = [&](const f32x16& s) {
-      float t0 = 0.f, t1 = 0.f, t2 = 0.f;
+      if constexpr (GK == 1 || GK == 2) {
+        int cnt = 0;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float zp = relu_z(c, s[r], tau);
-        if constexpr (GK == 1) {
-          t0 += zp;
-          t1 += ceilf(zp);
-        } else if constexpr (GK == 2) {
-          t0 = fmaf(zp, zp, t0);
-          t1 += zp;
-          t2 += ceilf(zp);
-        } else if constexpr (GK == 4) {
-          const float z2 = zp * zp;
-          t0 = fmaf(z2, z2, t0);
-          t1 = fmaf(z2, zp, t1);
-          t2 += z2;
-        } else {
-          if (zp > 0.f) {
-            const float l = __log2f(zp);
-            t0 += exp2f(g * l);
-            t1 += exp2f((g - 1.f) * l);
-            t2 += exp2f((g - 2.f) * l);
+        for (int r = 0; r < 16; r += 2) {
+          const float za = relu_z(c, s[r], tau), zb = relu_z(c, s[r + 1], tau);
+          if constexpr (GK == 1) {
+            m0 += za;
+            m0 += zb;
+          } else {
+            m0 = fmaf(za, za, m0);
+            m0 = fmaf(zb, zb, m0);
+            m1 += za;
+            m1 += zb;
+          }
+          cnt += in_support(za) + in_support(zb);
+        }
+        mc += cnt;
+        return cnt > 0;
+      } else {
+        float t0 = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float zp = relu_z(c, s[r], tau);
+          if constexpr (GK == 4) {
+            const float z2 = zp * zp;
+            t0 = fmaf(z2, z2, t0);
+            m1 = fmaf(z2, zp, m1);
+            m2 += z2;
+          } else {
+            if (zp > 0.f) {
+              const float l = __log2f(zp);
+              t0 += exp2f(g * l);
+              m1 += exp2f((g - 1.f) * l);
+              m2 += exp2f((g - 2.f) * l);
+            }
           }
         }
+        m0 += t0;
+        return t0 > 0.f;
       }
-      m0 += t0;
-      m1 += t1;
-      m2 += t2;
-      if constexpr (GK == 0) return t0 > 0.f;
-      else return (GK == 1 ? t1 : t2) > 0.f;
     };
+    uint32_t word = 0;  // mask bits of the current 32-block group (wave-uniform)
     stream([&](int kb, const E* kt) {
       const int j0 = kb * BLK;
       const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
-      if (k0 == 0 && k1 == 0) return;
-      f32x16 s0, s1;
-      scores(kt, s0, s1);
-      if (k0 == 2) mask_tile(s0, j0);
-      if (k1 == 2) mask_tile(s1, j0 + 32);
       bool any = false;
-      if (k0) any |= eval_tile(s0);
-      if (k1) any |= eval_tile(s1);
-      const unsigned long long hit = __ballot(any);
-      if (lane == 0) bits[w * MAX_KEY_BLOCKS + kb] = hit != 0ull;
+      if (k0 != 0 || k1 != 0) {
+        f32x16 s0, s1;
+        scores(kt, s0, s1);
+        if (k0 == 2) mask_tile(s0, j0);
+        if (k1 == 2) mask_tile(s1, j0 + 32);
+        if (k0) any |= eval_tile(s0);
+        if (k1) any |= eval_tile(s1);
+      }
+      if (__ballot(any) != 0ull) word |= 1u << (kb & 31);
+      if ((kb & 31) == 31 || kb == nkb - 1) {
+        if (lane == 0) bits[w * BW + (kb >> 5)] = word;
+        word = 0;
+      }
     });
     ++passes;
+    if constexpr (GK == 1) m1 = (float)mc;
+    if constexpr (GK == 2) m2 = (float)mc;
     m0 += __shfl_xor(m0, 32);
     m1 += __shfl_xor(m1, 32);
     m2 += __shfl_xor(m2, 32);
@@ -242,7 +264,8 @@ __global__ __launch_bounds__(TAU_NT) void tau_solve_kernel(TauArgs a) {
     const int half = x / T, kb = x % T;
     const int qb = QBLOCKS * qt + half;
     if (qb < T) {
-      const uint8_t b = bits[(2 * half) * MAX_KEY_BLOCKS + kb] | bits[(2 * half + 1) * MAX_KEY_BLOCKS + kb];
+      const uint32_t both = bits[(2 * half) * BW + (kb >> 5)] | bits[(2 * half + 1) * BW + (kb >> 5)];
+      const uint8_t b = (both >> (kb & 31)) & 1u;
       a.mask[((size_t)bh * T + qb) * T + kb] = b;
       if (a.stats && kb == 0) a.stats[(size_t)bh * T + qb] = passes;
     }
