@@ -38,7 +38,8 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
-__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+// Wave index within the workgroup, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 // Row of accumulator value r for the calling lane (see the layout note above).
 __device__ __forceinline__ int crow(int r) { return 8 * (r >> 2) + 4 * (lane_id() >> 5) + (r & 3); }
 

@@ -131,6 +131,11 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
     if (k0 == 0 && k1 == 0) return;
     f32x16 s0, s1;
     scores(kt, s0, s1);
+    if (k0 == 1 && k1 == 1) {
+      max_tile(s0);
+      max_tile(s1);
+      return;
+    }
     if (k0 == 2) mask_tile(s0, j0);
     if (k1 == 2) mask_tile(s1, j0 + 32);
     if (k0) max_tile(s0);
@@ -203,7 +208,13 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
       const int j0 = kb * BLK;
       const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
       bool any = false;
-      if (k0 != 0 || k1 != 0) {
+      if (k0 == 1 && k1 == 1) {  // every key valid: one straight-line block
+        f32x16 s0, s1;
+        scores(kt, s0, s1);
+        const bool a0 = eval_tile(s0);
+        const bool a1 = eval_tile(s1);
+        any = a0 || a1;
+      } else if (k0 != 0 || k1 != 0) {
         f32x16 s0, s1;
         scores(kt, s0, s1);
         if (k0 == 2) mask_tile(s0, j0);
