@@ -71,13 +71,23 @@ struct Mma<__bf16> {
     return f;
   }
   // Two-term split v ~ hi + lo, both bf16; hi + lo carries ~16 mantissa bits.
+  // Pairs are rounded together (one v_cvt_pk_bf16_f32); the fp32 values of
+  // the two hi halves come back out of the packed word with one shift and
+  // one mask, and the exact remainders are rounded as a second pair.
   __device__ __forceinline__ static void pack_split(const float* v, int t, frag& hi, frag& lo) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    u32x4 hw, lw;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      __bf16 h = (__bf16)v[8 * t + e];
-      hi[e] = h;
-      lo[e] = (__bf16)(v[8 * t + e] - (float)h);
+    for (int e = 0; e < 4; ++e) {
+      const float a = v[8 * t + 2 * e], b = v[8 * t + 2 * e + 1];
+      const uint32_t hp = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)a, (__bf16)b});
+      const float ra = a - __uint_as_float(hp << 16);
+      const float rb = b - __uint_as_float(hp & 0xFFFF0000u);
+      hw[e] = hp;
+      lw[e] = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)ra, (__bf16)rb});
     }
+    hi = __builtin_bit_cast(bf16x8, hw);
+    lo = __builtin_bit_cast(bf16x8, lw);
   }
   static constexpr bool exact_operands = false;
 };
