@@ -80,6 +80,7 @@ class Runner:
         self.dq, self.dk, self.dv = f32(), f32(), f32()
         self.ws = torch.empty(self.res.sizes.ws_bwd // 4 + 4, dtype=torch.float32,
                               device=self.q.device)
+        self.ws_fwd = ea.forward_workspace(self.res, self.q.device)
         self.events = [[torch.cuda.Event(enable_timing=True) for _ in range(7)]
                        for _ in range(max(1, args.steps))]
 
@@ -90,7 +91,8 @@ class Runner:
             ev[0].record()
         for st in range(3):
             ea._check(ea.entmax_attn_fwd_stage(st, self.shape, self.params, q, k, v,
-                                               self.o.data_ptr(), self.rp, s), "fwd stage")
+                                               self.o.data_ptr(), self.rp, self.ws_fwd.data_ptr(),
+                                               self.ws_fwd.numel(), s), "fwd stage")
             if ev:
                 ev[1 + st].record()
         for st in range(3):

@@ -87,7 +87,7 @@ typedef struct {
 /* Byte sizes of every residual buffer and of the workspaces. */
 typedef struct {
   size_t tau, o2, block_mask, q_count, q_index, k_count, k_index, stats;
-  size_t ws_fwd; /* workspace entmax_attn_fwd needs (currently 0) */
+  size_t ws_fwd; /* workspace entmax_attn_fwd can use: the solver's candidate cache */
   size_t ws_bwd; /* workspace entmax_attn_bwd needs: fp32 [BH, n] for delta */
 } ea_sizes;
 
@@ -105,7 +105,14 @@ ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_s
  *   q, k, v  [BH, n, d] in shape->dtype, 16-byte aligned
  *   o        [BH, n, d] in shape->dtype, 16-byte aligned (written)
  *   res      residual buffers (written), 4-byte aligned, o2 16-byte aligned
- *   workspace may be NULL when sizes.ws_fwd == 0
+ *   workspace optional, 16-byte aligned: the solver's candidate cache, one
+ *            256 KiB slot per 128-row query tile (sizes.ws_fwd covers all
+ *            tiles).  A tile with a slot, once its rows' brackets have
+ *            narrowed, stores the scores above each row's lower bracket end
+ *            and runs its remaining evaluations on them instead of
+ *            streaming K again; tiles without one (all of them for NULL)
+ *            stream K on every pass.  Results agree up to rounding either
+ *            way.  Contents are scratch.
  * Launches 3 kernels on `stream`.
  */
 ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const void* q,
@@ -139,7 +146,8 @@ ea_status entmax_attn_bwd(const ea_shape* shape, const ea_params* params, const 
  */
 ea_status entmax_attn_fwd_stage(int stage, const ea_shape* shape, const ea_params* params,
                                 const void* q, const void* k, const void* v, void* o,
-                                const ea_residuals* res, void* stream);
+                                const ea_residuals* res, void* workspace, size_t ws_bytes,
+                                void* stream);
 ea_status entmax_attn_bwd_stage(int stage, const ea_shape* shape, const ea_params* params,
                                 const void* q, const void* k, const void* v, const void* dout,
                                 const ea_residuals* res, float* dq, float* dk, float* dv,

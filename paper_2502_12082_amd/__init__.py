@@ -72,7 +72,7 @@ _lib.entmax_attn_bwd.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _P(Resid
                                  _v, _v, ctypes.c_size_t, _v]
 _lib.entmax_attn_bwd.restype = ctypes.c_int
 _lib.entmax_attn_fwd_stage.argtypes = [ctypes.c_int, _P(Shape), _P(Params), _v, _v, _v, _v,
-                                       _P(ResidualPtrs), _v]
+                                       _P(ResidualPtrs), _v, ctypes.c_size_t, _v]
 _lib.entmax_attn_fwd_stage.restype = ctypes.c_int
 _lib.entmax_attn_bwd_stage.argtypes = [ctypes.c_int, _P(Shape), _P(Params), _v, _v, _v, _v,
                                        _P(ResidualPtrs), _v, _v, _v, _v, ctypes.c_size_t, _v]
@@ -125,9 +125,10 @@ def entmax_attn_bwd(shape, params, q, k, v, dout, res: ResidualPtrs, dq, dk, dv,
                                 ctypes.byref(res), dq, dk, dv, workspace, ws_bytes, stream)
 
 
-def entmax_attn_fwd_stage(stage, shape, params, q, k, v, o, res: ResidualPtrs, stream):
+def entmax_attn_fwd_stage(stage, shape, params, q, k, v, o, res: ResidualPtrs, workspace,
+                          ws_bytes, stream):
     return _lib.entmax_attn_fwd_stage(stage, ctypes.byref(shape), ctypes.byref(params), q, k, v,
-                                      o, ctypes.byref(res), stream)
+                                      o, ctypes.byref(res), workspace, ws_bytes, stream)
 
 
 def entmax_attn_bwd_stage(stage, shape, params, q, k, v, dout, res: ResidualPtrs, dq, dk, dv,
@@ -196,9 +197,17 @@ def _stream_handle(device):
     return torch.cuda.current_stream(device).cuda_stream
 
 
+def forward_workspace(res: Residuals, device):
+    """A device buffer of sizes.ws_fwd bytes for the solver's candidate cache."""
+    return torch.empty(max(res.sizes.ws_fwd, 16), dtype=torch.uint8, device=device)
+
+
 def forward(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_iter=None,
-            tol=None, out=None, res: Residuals | None = None):
-    """O and the residuals for Q, K, V ([B, H, n, d] bf16/fp32 CUDA tensors)."""
+            tol=None, out=None, res: Residuals | None = None, workspace=None):
+    """O and the residuals for Q, K, V ([B, H, n, d] bf16/fp32 CUDA tensors).
+
+    workspace: a uint8 device tensor for the solver's candidate cache (None
+    allocates sizes.ws_fwd bytes; False runs the solver without the cache)."""
     for t in (q, k, v):
         if not t.is_cuda or not t.is_contiguous() or t.shape != q.shape or t.dtype != q.dtype:
             raise ValueError("q, k, v must be contiguous device tensors of one shape and dtype")
@@ -209,8 +218,12 @@ def forward(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_ite
     if out is None:
         out = torch.empty_like(q)
     rp = res.ptrs()
+    if workspace is None:
+        workspace = forward_workspace(res, q.device)
+    ws_ptr, ws_bytes = (None, 0) if workspace is False else (workspace.data_ptr(),
+                                                            workspace.numel() * workspace.element_size())
     _check(entmax_attn_fwd(shape, params, q.data_ptr(), k.data_ptr(), v.data_ptr(),
-                           out.data_ptr(), rp, None, 0, _stream_handle(q.device)),
+                           out.data_ptr(), rp, ws_ptr, ws_bytes, _stream_handle(q.device)),
            "entmax_attn_fwd")
     res.params = params
     return out, res

@@ -21,6 +21,9 @@ namespace {
 constexpr int DEFAULT_MAX_ITER = 12;
 constexpr float DEFAULT_TOL = 1e-5f;
 constexpr int MAX_ITER_CAP = 64;
+// Candidate-cache entries per solver thread (see entmax_attn_sizes).
+constexpr int TAU_CACHE_CAP = 128;
+constexpr size_t TAU_SLOT_BYTES = (size_t)TAU_CACHE_CAP * TAU_THREADS * sizeof(CandEntry);
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -57,6 +60,12 @@ ea_status check_shape(const ea_shape* s, const ea_params* p, Dims* out) {
   return EA_OK;
 }
 
+// delta, one fp32 per row
+size_t bwd_ws_bytes(const Dims& d) { return (size_t)(d.BH * d.n) * 4; }
+
+// One cache slot per 128-row solver tile.
+int64_t cache_slots(const Dims& d) { return d.BH * ((d.n + TAU_ROWS - 1) / TAU_ROWS); }
+
 void fill_sizes(const Dims& d, ea_sizes* z) {
   z->tau = (size_t)(d.BH * d.n) * 4;
   z->o2 = (size_t)d.elems * 4;
@@ -66,8 +75,8 @@ void fill_sizes(const Dims& d, ea_sizes* z) {
   z->k_count = z->q_count;
   z->k_index = z->q_index;
   z->stats = (size_t)(d.BH * d.T) * 4;
-  z->ws_fwd = 0;
-  z->ws_bwd = (size_t)(d.BH * d.n) * 4;
+  z->ws_fwd = (size_t)cache_slots(d) * TAU_SLOT_BYTES;
+  z->ws_bwd = bwd_ws_bytes(d);
 }
 
 bool tensor_ok(const void* p) { return p && aligned(p, 16); }
@@ -121,9 +130,11 @@ namespace {
 
 // Checks shared by the forward entry points; fills the kernel arguments.
 ea_status prep_fwd(const ea_shape* shape, const ea_params* params, const void* q, const void* k,
-                   const void* v, void* o, const ea_residuals* res, Dims* d) {
+                   const void* v, void* o, const ea_residuals* res, const void* workspace,
+                   Dims* d) {
   ea_status st = check_shape(shape, params, d);
   if (st != EA_OK) return st;
+  if (workspace && !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
   if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(o)) return EA_ERR_INVALID_ARG;
   if ((st = check_tables(res)) != EA_OK) return st;
   if (params->need_bwd && !tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
@@ -132,13 +143,20 @@ ea_status prep_fwd(const ea_shape* shape, const ea_params* params, const void* q
 
 ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const void* q,
                         const void* k, const void* v, void* o, const ea_residuals* res,
-                        hipStream_t s) {
+                        void* workspace, size_t ws_bytes, hipStream_t s) {
   const float c = (params->alpha - 1.0f) * params->scale;
   const float gamma = 1.0f / (params->alpha - 1.0f);
   const int gk = gamma_kind(params->alpha);
   if (stage == 0) {
-    TauArgs ta{q, k, res->tau, res->block_mask, res->stats, (int)d.BH, (int)d.n, (int)d.T,
-               c, params->alpha, gamma, params->causal, params->max_iter, params->tol, gk};
+    // The cache is optional: tiles without a slot (all of them when there is
+    // no workspace) stream K on every solver pass.
+    int64_t slots = workspace ? (int64_t)(ws_bytes / TAU_SLOT_BYTES) : 0;
+    const int64_t most = cache_slots(d);
+    if (slots > most) slots = most;
+    CandEntry* cand = slots > 0 ? static_cast<CandEntry*>(workspace) : nullptr;
+    TauArgs ta{q, k, res->tau, res->block_mask, res->stats, cand, TAU_CACHE_CAP, (int)slots,
+               (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma, params->causal,
+               params->max_iter, params->tol, gk};
     return from_hip(launch_tau(ta, d.dtype, (int)d.d, s));
   }
   if (stage == 1) {
@@ -161,10 +179,8 @@ ea_status prep_bwd(const ea_shape* shape, const ea_params* params, const void* q
   if (!tensor_ok(dq) || !tensor_ok(dk) || !tensor_ok(dv)) return EA_ERR_INVALID_ARG;
   if ((st = check_tables(res)) != EA_OK) return st;
   if (!tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
-  ea_sizes z;
-  fill_sizes(*d, &z);
   if (!workspace || !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
-  if (ws_bytes < z.ws_bwd) return EA_ERR_WORKSPACE;
+  if (ws_bytes < bwd_ws_bytes(*d)) return EA_ERR_WORKSPACE;
   return EA_OK;
 }
 
@@ -190,25 +206,26 @@ ea_status run_bwd_stage(int stage, const Dims& d, const ea_params* params, const
 ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const void* q,
                           const void* k, const void* v, void* o, const ea_residuals* res,
                           void* workspace, size_t ws_bytes, void* stream) {
-  (void)workspace;
-  (void)ws_bytes;
   Dims d;
-  ea_status st = prep_fwd(shape, params, q, k, v, o, res, &d);
+  ea_status st = prep_fwd(shape, params, q, k, v, o, res, workspace, &d);
   if (st != EA_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   for (int stage = 0; stage < 3; ++stage)
-    if ((st = run_fwd_stage(stage, d, params, q, k, v, o, res, s)) != EA_OK) return st;
+    if ((st = run_fwd_stage(stage, d, params, q, k, v, o, res, workspace, ws_bytes, s)) != EA_OK)
+      return st;
   return EA_OK;
 }
 
 ea_status entmax_attn_fwd_stage(int stage, const ea_shape* shape, const ea_params* params,
                                 const void* q, const void* k, const void* v, void* o,
-                                const ea_residuals* res, void* stream) {
+                                const ea_residuals* res, void* workspace, size_t ws_bytes,
+                                void* stream) {
   if (stage < 0 || stage > 2) return EA_ERR_INVALID_ARG;
   Dims d;
-  ea_status st = prep_fwd(shape, params, q, k, v, o, res, &d);
+  ea_status st = prep_fwd(shape, params, q, k, v, o, res, workspace, &d);
   if (st != EA_OK) return st;
-  return run_fwd_stage(stage, d, params, q, k, v, o, res, static_cast<hipStream_t>(stream));
+  return run_fwd_stage(stage, d, params, q, k, v, o, res, workspace, ws_bytes,
+                       static_cast<hipStream_t>(stream));
 }
 
 ea_status entmax_attn_bwd(const ea_shape* shape, const ea_params* params, const void* q,

@@ -16,12 +16,26 @@ constexpr int MAX_KEY_BLOCKS = MAX_SEQLEN / 64;
 // {1, 2, 4} run without transcendentals; 0 means general alpha.
 int gamma_kind(float alpha);
 
+// One cached score of the solver: x = (alpha-1) * scale * <q_i, k_j> and the
+// key block of j.
+struct alignas(8) CandEntry {
+  float x;
+  int32_t kb;
+};
+
+// Solver workgroup geometry (rows per workgroup, threads per workgroup).
+constexpr int TAU_ROWS = 128;
+constexpr int TAU_THREADS = 256;
+
 struct TauArgs {
   const void* q;
   const void* k;
   float* tau;         // [BH, n]
   uint8_t* mask;      // [BH, T, T]
   int32_t* stats;     // [BH, T] K passes run for each 64-row query block, or null
+  CandEntry* cand;    // candidate cache: [slots][cap][TAU_THREADS], or null
+  int cap;            // entries per thread
+  int slots;          // 128-row tiles with a cache slot (tile t uses slot t)
   int BH, n, T;
   float c;            // (alpha - 1) * scale
   float alpha, gamma;

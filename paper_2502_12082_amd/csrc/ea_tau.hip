@@ -41,252 +41,350 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
   constexpr int BW = MAX_KEY_BLOCKS / 32;  // mask words per wave
   __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
   // bit kb of word kb / 32: key block kb holds a positive probability for
-  // one of the wave's 32 rows (written by the wave's lane 0 only)
+  // one of the wave's 32 rows
   __shared__ uint32_t bits[TAU_WAVES * BW];
 
   const int lane = lane_id(), w = wave_id();
   const int n = a.n, T = a.T;
   const int nqt = (n + TAU_ROWS - 1) / TAU_ROWS;
-  const int bh = blockIdx.x % a.BH;
-  int qt = blockIdx.x / a.BH;
-  if (a.causal) qt = nqt - 1 - qt;  // longest rows first
-  const int q0 = qt * TAU_ROWS + 32 * w;
-  const int i = q0 + (lane & 31);
-  const bool row_ok = i < n;
-  const int ni = a.causal ? i + 1 : n;
-  const E* Q = static_cast<const E*>(a.q) + (size_t)bh * n * D;
-  const E* K = static_cast<const E*>(a.k) + (size_t)bh * n * D;
-
-  const int wg_last = min(n, (qt + 1) * TAU_ROWS) - 1;
-  const int nkb = a.causal ? wg_last / BLK + 1 : T;
-  const int wave_last = min(n - 1, q0 + 31);
-  const bool wave_ok = q0 < n;
-
-  typename M::frag qf[KS];
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) qf[kk] = load_row_frag_global<E, D>(Q, i, n, kk);
-
   const int TW = (T + 31) / 32;
-  for (int x = threadIdx.x; x < TAU_WAVES * TW; x += TAU_NT) bits[(x / TW) * BW + (x % TW)] = 0;
+  const float c = a.c, g = a.gamma;
+  // The Newton step from any tau is a lower bound of the root when f is
+  // convex, i.e. gamma >= 1 (alpha <= 2).
+  const bool newton_bound = g >= 1.f;
+  // This workgroup's slot of the candidate cache (entry e of thread t at
+  // [e * TAU_NT + t]), or null when the workspace has no slot for it.
+  const int tile = blockIdx.x;
+  CandEntry* const cache =
+      a.cand && tile < a.slots ? a.cand + (size_t)tile * a.cap * TAU_NT : nullptr;
 
-  const float c = a.c;
-
-  // Streams every key block the workgroup needs, double-buffered: block
-  // kb + 1 is copied into LDS while `body(kb, tile)` works on block kb.
   TileDma<TL, D, TAU_NT> dma;
   dma.init();
-  auto stream = [&](auto&& body) {
-    dma.issue(kbuf[0], K, 0, n);
-    for (int kb = 0; kb < nkb; ++kb) {
-      dma_wait();
-      __syncthreads();
-      if (kb + 1 < nkb) dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
-      body(kb, kbuf[kb & 1]);
-    }
-    __syncthreads();  // the next pass refills buffer 0
-  };
 
-  // S^T sub-tiles of the staged block: keys [0, 32) and [32, 64) x this
-  // wave's 32 queries; value r of lane l is key 32 sub + crow(r), query l%32.
-  // The two accumulation chains are interleaved so neither waits on the
-  // other; both are computed whenever the block has a valid key (a half with
-  // none is then simply not used).
-  auto scores = [&](const E* kt, f32x16& s0, f32x16& s1) {
-    s0 = zero16();
-    s1 = zero16();
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      const typename M::frag a0 = lds_row_frag_pad<E, D>(kt, (lane & 31), kk);
-      const typename M::frag a1 = lds_row_frag_pad<E, D>(kt, 32 + (lane & 31), kk);
-      s0 = M::mma(a0, qf[kk], s0);
-      s1 = M::mma(a1, qf[kk], s1);
-    }
-  };
-  // Sub-tile state for the calling wave: 0 = nothing valid, 1 = all valid,
-  // 2 = needs per-element masking (ragged tail or causal diagonal).
-  auto sub_kind = [&](int j0) {
-    if (!wave_ok || j0 >= n || (a.causal && j0 > wave_last)) return 0;
-    if (j0 + 31 >= n || (a.causal && j0 + 31 > q0)) return 2;
-    return 1;
-  };
-  auto valid = [&](int j) { return j < n && (!a.causal || j <= i); };
+  {
+    const int bh = tile % a.BH;
+    int qt = tile / a.BH;
+    if (a.causal) qt = nqt - 1 - qt;  // longest rows first
+    const int q0 = qt * TAU_ROWS + 32 * w;
+    const int i = q0 + (lane & 31);
+    const bool row_ok = i < n;
+    const int ni = a.causal ? i + 1 : n;
+    const E* Q = static_cast<const E*>(a.q) + (size_t)bh * n * D;
+    const E* K = static_cast<const E*>(a.k) + (size_t)bh * n * D;
 
-  // ---- pass 0: row maximum of the raw scores (scale > 0, so the maximum of
-  // x = c s is c times the maximum of s)
-  float smax = -INFINITY;
-  // Invalid keys of a masked sub-tile become -inf: they cannot be the
-  // maximum, and the clamp of [x - tau]_+ turns them into exactly 0.
-  auto mask_tile = [&](f32x16& s, int j0) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r)
-      if (!valid(j0 + crow(r))) s[r] = -INFINITY;
-  };
-  auto max_tile = [&](const f32x16& s) {
-#pragma unroll
-    for (int r = 0; r < 16; r += 2) smax = fmaxf(smax, fmaxf(s[r], s[r + 1]));
-  };
-  stream([&](int kb, const E* kt) {
-    const int j0 = kb * BLK;
-    const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
-    if (k0 == 0 && k1 == 0) return;
-    f32x16 s0, s1;
-    scores(kt, s0, s1);
-    if (k0 == 1 && k1 == 1) {
-      max_tile(s0);
-      max_tile(s1);
-      return;
-    }
-    if (k0 == 2) mask_tile(s0, j0);
-    if (k1 == 2) mask_tile(s1, j0 + 32);
-    if (k0) max_tile(s0);
-    if (k1) max_tile(s1);
-  });
-  smax = fmaxf(smax, __shfl_xor(smax, 32));
+    const int wg_last = min(n, (qt + 1) * TAU_ROWS) - 1;
+    const int nkb = a.causal ? wg_last / BLK + 1 : T;
+    const int wave_last = min(n - 1, q0 + 31);
+    const bool wave_ok = q0 < n;
 
-  float lo = 0.f, hi = 0.f, tau = 0.f;
-  if (row_ok) {
-    const float m = c * smax;
-    lo = m - 1.f;
-    hi = m - powf((float)ni, 1.f - a.alpha);
-    tau = 0.5f * (lo + hi);
-  }
+    typename M::frag qf[KS];
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) qf[kk] = load_row_frag_global<E, D>(Q, i, n, kk);
 
-  const float g = a.gamma;
-  int passes = 1;
-  for (int it = 0;; ++it) {
-    // ---- evaluation pass at tau: m0 = sum z^gamma, m1 = sum z^(gamma-1),
-    // m2 = sum z^(gamma-2) over the strict support z > 0.  For gamma = 1, 2
-    // the last of these is the size of the support, counted exactly as an
-    // integer (mc).
-    float m0 = 0.f, m1 = 0.f, m2 = 0.f;
-    int mc = 0;
-    // Adds one sub-tile; returns whether it holds a positive probability.
-    auto eval_tile = [&](const f32x16& s) {
-      if constexpr (GK == 1 || GK == 2) {
-        int cnt = 0;
+    for (int x = threadIdx.x; x < TAU_WAVES * TW; x += TAU_NT) bits[(x / TW) * BW + (x % TW)] = 0;
+
+    // Streams every key block the tile needs, double-buffered: block kb + 1
+    // is copied into LDS while `body(kb, tile)` works on block kb.
+    auto stream = [&](auto&& body) {
+      dma.issue(kbuf[0], K, 0, n);
+      for (int kb = 0; kb < nkb; ++kb) {
+        dma_wait();
+        __syncthreads();
+        if (kb + 1 < nkb) dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
+        body(kb, kbuf[kb & 1]);
+      }
+      __syncthreads();  // the next pass refills buffer 0
+    };
+
+    // S^T sub-tiles of the staged block: keys [0, 32) and [32, 64) x this
+    // wave's 32 queries; value r of lane l is key 32 sub + crow(r), query
+    // l%32.  The two accumulation chains are interleaved so neither waits on
+    // the other.
+    auto scores = [&](const E* kt, f32x16& s0, f32x16& s1) {
+      s0 = zero16();
+      s1 = zero16();
 #pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-          const float za = relu_z(c, s[r], tau), zb = relu_z(c, s[r + 1], tau);
-          if constexpr (GK == 1) {
-            m0 += za;
-            m0 += zb;
-          } else {
-            m0 = fmaf(za, za, m0);
-            m0 = fmaf(zb, zb, m0);
-            m1 += za;
-            m1 += zb;
-          }
-          cnt += in_support(za) + in_support(zb);
-        }
-        mc += cnt;
-        return cnt > 0;
-      } else {
-        float t0 = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float zp = relu_z(c, s[r], tau);
-          if constexpr (GK == 4) {
-            const float z2 = zp * zp;
-            t0 = fmaf(z2, z2, t0);
-            m1 = fmaf(z2, zp, m1);
-            m2 += z2;
-          } else {
-            if (zp > 0.f) {
-              const float l = __log2f(zp);
-              t0 += exp2f(g * l);
-              m1 += exp2f((g - 1.f) * l);
-              m2 += exp2f((g - 2.f) * l);
-            }
-          }
-        }
-        m0 += t0;
-        return t0 > 0.f;
+      for (int kk = 0; kk < KS; ++kk) {
+        const typename M::frag a0 = lds_row_frag_pad<E, D>(kt, (lane & 31), kk);
+        const typename M::frag a1 = lds_row_frag_pad<E, D>(kt, 32 + (lane & 31), kk);
+        s0 = M::mma(a0, qf[kk], s0);
+        s1 = M::mma(a1, qf[kk], s1);
       }
     };
-    uint32_t word = 0;  // mask bits of the current 32-block group (wave-uniform)
+    // Sub-tile state for the calling wave: 0 = nothing valid, 1 = all valid,
+    // 2 = needs per-element masking (ragged tail or causal diagonal).
+    auto sub_kind = [&](int j0) {
+      if (!wave_ok || j0 >= n || (a.causal && j0 > wave_last)) return 0;
+      if (j0 + 31 >= n || (a.causal && j0 + 31 > q0)) return 2;
+      return 1;
+    };
+    auto valid = [&](int j) { return j < n && (!a.causal || j <= i); };
+    // Invalid keys of a masked sub-tile become -inf: they cannot be the
+    // maximum, and the clamp of [x - tau]_+ turns them into exactly 0.
+    auto mask_tile = [&](f32x16& s, int j0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (!valid(j0 + crow(r))) s[r] = -INFINITY;
+    };
+
+    // ---- pass 0: row maximum of the raw scores (scale > 0, so the maximum
+    // of x = c s is c times the maximum of s)
+    float smax = -INFINITY;
+    auto max_tile = [&](const f32x16& s) {
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) smax = fmaxf(smax, fmaxf(s[r], s[r + 1]));
+    };
     stream([&](int kb, const E* kt) {
       const int j0 = kb * BLK;
       const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
-      bool any = false;
-      if (k0 == 1 && k1 == 1) {  // every key valid: one straight-line block
-        f32x16 s0, s1;
-        scores(kt, s0, s1);
-        const bool a0 = eval_tile(s0);
-        const bool a1 = eval_tile(s1);
-        any = a0 || a1;
-      } else if (k0 != 0 || k1 != 0) {
-        f32x16 s0, s1;
-        scores(kt, s0, s1);
-        if (k0 == 2) mask_tile(s0, j0);
-        if (k1 == 2) mask_tile(s1, j0 + 32);
-        if (k0) any |= eval_tile(s0);
-        if (k1) any |= eval_tile(s1);
+      if (k0 == 0 && k1 == 0) return;
+      f32x16 s0, s1;
+      scores(kt, s0, s1);
+      if (k0 == 1 && k1 == 1) {
+        max_tile(s0);
+        max_tile(s1);
+        return;
       }
-      if (__ballot(any) != 0ull) word |= 1u << (kb & 31);
-      if ((kb & 31) == 31 || kb == nkb - 1) {
-        if (lane == 0) bits[w * BW + (kb >> 5)] = word;
-        word = 0;
-      }
+      if (k0 == 2) mask_tile(s0, j0);
+      if (k1 == 2) mask_tile(s1, j0 + 32);
+      if (k0) max_tile(s0);
+      if (k1) max_tile(s1);
     });
-    ++passes;
-    if constexpr (GK == 1) m1 = (float)mc;
-    if constexpr (GK == 2) m2 = (float)mc;
-    m0 += __shfl_xor(m0, 32);
-    m1 += __shfl_xor(m1, 32);
-    m2 += __shfl_xor(m2, 32);
+    smax = fmaxf(smax, __shfl_xor(smax, 32));
 
-    const float f = m0 - 1.f;                        // Eq. 3
-    float f1, f2;                                    // Eq. 6, 7
-    if constexpr (GK == 1) {
-      f1 = -m1;
-      f2 = 0.f;
-    } else if constexpr (GK == 2) {
-      f1 = -2.f * m1;
-      f2 = 2.f * m2;
-    } else if constexpr (GK == 4) {
-      f1 = -4.f * m1;
-      f2 = 12.f * m2;
-    } else {
-      f1 = -g * m1;
-      f2 = g * (g - 1.f) * m2;
-    }
-    const bool conv = !row_ok || fabsf(f) <= a.tol;
-    if (__syncthreads_and(conv) || it >= a.max_iter) break;
+    float lo = 0.f, hi = 0.f, tau = 0.f;
     if (row_ok) {
-      if (f < 0.f)  // B_f, Eq. 4 ("otherwise" branch when f == 0)
-        hi = tau;
-      else
-        lo = tau;
-      const float th = tau - 2.f * f * f1 / (2.f * f1 * f1 - f * f2);  // H_f, Eq. 5
-      // Bracket test of Algorithm 1 with fp32 rounding: when the root sits on
-      // an end of the bracket (one-hot rows: tau = max - 1; constant rows:
-      // tau = max - n^(1-alpha)) the Halley value lands within a few ulps on
-      // either side of it, so values within `slack` are accepted and clamped
-      // into [lo, hi].  NaN and inf fail the test and take the midpoint.
-      const float slack = 1e-6f * fmaxf(1.f, fmaxf(fabsf(lo), fabsf(hi)));
-      tau = (th >= lo - slack && th <= hi + slack) ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
+      const float m = c * smax;
+      lo = m - 1.f;
+      hi = m - powf((float)ni, 1.f - a.alpha);
+      tau = 0.5f * (lo + hi);
     }
-  }
 
-  if (row_ok && lane < 32) a.tau[(size_t)bh * n + i] = tau;
-  __syncthreads();
-  constexpr int QBLOCKS = TAU_WAVES / 2;  // 64-row mask rows per workgroup
-  for (int x = threadIdx.x; x < QBLOCKS * T; x += TAU_NT) {
-    const int half = x / T, kb = x % T;
-    const int qb = QBLOCKS * qt + half;
-    if (qb < T) {
-      const uint32_t both = bits[(2 * half) * BW + (kb >> 5)] | bits[(2 * half + 1) * BW + (kb >> 5)];
-      const uint8_t b = (both >> (kb & 31)) & 1u;
-      a.mask[((size_t)bh * T + qb) * T + kb] = b;
-      if (a.stats && kb == 0) a.stats[(size_t)bh * T + qb] = passes;
+    int passes = 1;      // K passes (streamed), the max pass included
+    bool cached = false; // evaluations run on the candidate cache
+    int attempts = 0;    // cache fills tried
+    int cc = 0;          // candidates this thread found in the last fill
+    int cmax = 0;        // wave maximum of cc once the cache is in use
+    bool small_support = false;  // every thread's support count <= cap / 2
+    for (int it = 0;; ++it) {
+      // ---- evaluation at tau: m0 = sum z^gamma, m1 = sum z^(gamma-1),
+      // m2 = sum z^(gamma-2) over the strict support z > 0, and mc = the size
+      // of the support (for gamma = 1, 2 that is the last sum, counted exactly
+      // as an integer).
+      float m0 = 0.f, m1 = 0.f, m2 = 0.f;
+      int mc = 0;
+      // Adds the terms of one value z = [x - tau]_+ (clamped to [0, 1]) to
+      // (t0, t1, t2, tc).
+      auto add_z = [&](float zp, float& t0, float& t1, float& t2, int& tc) {
+        if constexpr (GK == 1) {
+          t0 += zp;
+          tc += in_support(zp);
+        } else if constexpr (GK == 2) {
+          t0 = fmaf(zp, zp, t0);
+          t1 += zp;
+          tc += in_support(zp);
+        } else if constexpr (GK == 4) {
+          const float z2 = zp * zp;
+          t0 = fmaf(z2, z2, t0);
+          t1 = fmaf(z2, zp, t1);
+          t2 += z2;
+          tc += in_support(zp);
+        } else {
+          if (zp > 0.f) {
+            const float l = __log2f(zp);
+            t0 += exp2f(g * l);
+            t1 += exp2f((g - 1.f) * l);
+            t2 += exp2f((g - 2.f) * l);
+            ++tc;
+          }
+        }
+      };
+      // Adds one sub-tile; returns whether it holds a positive probability.
+      auto eval_tile = [&](const f32x16& s) {
+        if constexpr (GK == 1 || GK == 2) {
+          int cnt = 0;
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) {
+            const float za = relu_z(c, s[r], tau), zb = relu_z(c, s[r + 1], tau);
+            if constexpr (GK == 1) {
+              m0 += za;
+              m0 += zb;
+            } else {
+              m0 = fmaf(za, za, m0);
+              m0 = fmaf(zb, zb, m0);
+              m1 += za;
+              m1 += zb;
+            }
+            cnt += in_support(za) + in_support(zb);
+          }
+          mc += cnt;
+          return cnt > 0;
+        } else {
+          // tile sums start from 0, so t0 > 0 exactly when some term is > 0
+          float t0 = 0.f;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) add_z(relu_z(c, s[r], tau), t0, m1, m2, mc);
+          m0 += t0;
+          return t0 > 0.f;
+        }
+      };
+      // Appends the entries x > lo of a sub-tile to this thread's cache list.
+      // Every later tau stays >= lo, so the entries left out are 0 there.
+      const float s_lo = row_ok ? lo / c : INFINITY;  // rows past n collect nothing
+      CandEntry* const mine = cache + threadIdx.x;
+      auto fill_tile = [&](const f32x16& s, int kb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          if (s[r] > s_lo) {
+            if (cc < a.cap) mine[cc * TAU_NT] = CandEntry{c * s[r], kb};
+            ++cc;
+          }
+        }
+      };
+
+      // From the second evaluation on, a tile with a cache slot tries (at
+      // most twice) to collect its candidates x > lo in a K pass of their
+      // own, when the last streamed evaluation suggests that they fit; the
+      // evaluation at tau then runs on the cache.  If a thread's list
+      // overflows, this evaluation streams K as usual.
+      if (!cached && cache && it >= 1 && attempts < 2 && small_support) {
+        ++attempts;
+        cc = 0;
+        stream([&](int kb, const E* kt) {
+          const int j0 = kb * BLK;
+          const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
+          if (k0 == 0 && k1 == 0) return;
+          f32x16 s0, s1;
+          scores(kt, s0, s1);
+          if (k0 == 2) mask_tile(s0, j0);
+          if (k1 == 2) mask_tile(s1, j0 + 32);
+          if (k0) fill_tile(s0, kb);
+          if (k1) fill_tile(s1, kb);
+        });
+        ++passes;
+        if (!__syncthreads_or(cc > a.cap)) {
+          cached = true;
+          cmax = cc;
+#pragma unroll
+          for (int o = 32; o >= 1; o >>= 1) cmax = max(cmax, __shfl_xor(cmax, o));
+        }
+      }
+      if (!cached) {
+        // streamed evaluation; the mask bits of every block are rewritten
+        uint32_t word = 0;  // mask bits of the current 32-block group (wave-uniform)
+        stream([&](int kb, const E* kt) {
+          const int j0 = kb * BLK;
+          const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
+          bool any = false;
+          if (k0 == 1 && k1 == 1) {  // every key valid: one straight-line block
+            f32x16 s0, s1;
+            scores(kt, s0, s1);
+            const bool a0 = eval_tile(s0);
+            const bool a1 = eval_tile(s1);
+            any = a0 || a1;
+          } else if (k0 != 0 || k1 != 0) {
+            f32x16 s0, s1;
+            scores(kt, s0, s1);
+            if (k0 == 2) mask_tile(s0, j0);
+            if (k1 == 2) mask_tile(s1, j0 + 32);
+            if (k0) any |= eval_tile(s0);
+            if (k1) any |= eval_tile(s1);
+          }
+          if (__ballot(any) != 0ull) word |= 1u << (kb & 31);
+          if ((kb & 31) == 31 || kb == nkb - 1) {
+            if (lane == 0) bits[w * BW + (kb >> 5)] = word;
+            word = 0;
+          }
+        });
+        ++passes;
+        // support sizes at this tau, a guide to the size of the candidate lists
+        small_support = !__syncthreads_or(mc > a.cap / 2);
+      } else {
+        // cached evaluation: the same sums over this thread's list
+        for (int e = 0; e < cmax; ++e) {
+          if (e < cc) {
+            const CandEntry ce = cache[(size_t)e * TAU_NT + threadIdx.x];
+            add_z(__builtin_amdgcn_fmed3f(ce.x - tau, 0.f, 1.f), m0, m1, m2, mc);
+          }
+        }
+      }
+      if constexpr (GK == 1) m1 = (float)mc;
+      if constexpr (GK == 2) m2 = (float)mc;
+      m0 += __shfl_xor(m0, 32);
+      m1 += __shfl_xor(m1, 32);
+      m2 += __shfl_xor(m2, 32);
+
+      const float f = m0 - 1.f;                        // Eq. 3
+      float f1, f2;                                    // Eq. 6, 7
+      if constexpr (GK == 1) {
+        f1 = -m1;
+        f2 = 0.f;
+      } else if constexpr (GK == 2) {
+        f1 = -2.f * m1;
+        f2 = 2.f * m2;
+      } else if constexpr (GK == 4) {
+        f1 = -4.f * m1;
+        f2 = 12.f * m2;
+      } else {
+        f1 = -g * m1;
+        f2 = g * (g - 1.f) * m2;
+      }
+      const bool conv = !row_ok || fabsf(f) <= a.tol;
+      if (__syncthreads_and(conv) || it >= a.max_iter) break;
+      if (row_ok) {
+        if (f < 0.f)  // B_f, Eq. 4 ("otherwise" branch when f == 0)
+          hi = tau;
+        else
+          lo = tau;
+        // Bracket test of Algorithm 1 with fp32 rounding: when the root sits
+        // on an end of the bracket (one-hot rows: tau = max - 1; constant
+        // rows: tau = max - n^(1-alpha)) the Halley value lands within a few
+        // ulps on either side of it, so values within `slack` are accepted
+        // and clamped into [lo, hi].  NaN and inf fail the test and take the
+        // midpoint.
+        const float slack = 1e-6f * fmaxf(1.f, fmaxf(fabsf(lo), fabsf(hi)));
+        if (newton_bound && f1 < 0.f) {
+          // convexity: the tangent at tau meets zero at or below the root;
+          // a margin of 10 slacks covers the rounding of that point
+          const float tn = tau - f / f1 - 10.f * slack;
+          lo = fminf(fmaxf(lo, tn), hi);
+        }
+        const float th = tau - 2.f * f * f1 / (2.f * f1 * f1 - f * f2);  // H_f, Eq. 5
+        tau = (th >= lo - slack && th <= hi + slack) ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
+      }
+    }
+
+    if (cached) {
+      // mask bits at the returned tau from the cached entries
+      for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
+      __syncthreads();
+      for (int e = 0; e < cmax; ++e) {
+        if (e < cc) {
+          const CandEntry ce = cache[(size_t)e * TAU_NT + threadIdx.x];
+          if (ce.x - tau > 0.f) atomicOr(&bits[w * BW + (ce.kb >> 5)], 1u << (ce.kb & 31));
+        }
+      }
+    }
+
+    if (row_ok && lane < 32) a.tau[(size_t)bh * n + i] = tau;
+    __syncthreads();
+    constexpr int QBLOCKS = TAU_WAVES / 2;  // 64-row mask rows per workgroup
+    for (int x = threadIdx.x; x < QBLOCKS * T; x += TAU_NT) {
+      const int half = x / T, kb = x % T;
+      const int qb = QBLOCKS * qt + half;
+      if (qb < T) {
+        const uint32_t both = bits[(2 * half) * BW + (kb >> 5)] | bits[(2 * half + 1) * BW + (kb >> 5)];
+        const uint8_t b = (both >> (kb & 31)) & 1u;
+        a.mask[((size_t)bh * T + qb) * T + kb] = b;
+        if (a.stats && kb == 0) a.stats[(size_t)bh * T + qb] = passes;
+      }
     }
   }
 }
 
 template <typename E, int D>
 hipError_t launch_tau_d(const TauArgs& a, hipStream_t s) {
-  const int nqt = (a.n + TAU_ROWS - 1) / TAU_ROWS;
-  dim3 grid((unsigned)(a.BH * nqt)), block(TAU_NT);
+  dim3 grid((unsigned)(a.BH * ((a.n + TAU_ROWS - 1) / TAU_ROWS))), block(TAU_NT);
   auto kernel = tau_solve_kernel<E, D, 0>;
   if (a.gk == 1) kernel = tau_solve_kernel<E, D, 1>;
   if (a.gk == 2) kernel = tau_solve_kernel<E, D, 2>;

@@ -54,7 +54,9 @@ def test_sizes():
     assert z.q_count == z.k_count == BH * T * 4
     assert z.q_index == z.k_index == BH * T * T * 4
     assert z.stats == BH * T * 4
-    assert z.ws_fwd == 0 and z.ws_bwd == BH * n * 4
+    # solver cache: whole slots of 128 entries x 256 threads x 8 bytes (no
+    # slots without a device to size them for)
+    assert z.ws_fwd % (128 * 256 * 8) == 0 and z.ws_bwd == BH * n * 4
 
 
 @pytest.mark.parametrize("field,value,code", [
