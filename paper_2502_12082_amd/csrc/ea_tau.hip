@@ -166,6 +166,7 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
     int cc = 0;          // candidates this thread found in the last fill
     int cmax = 0;        // wave maximum of cc once the cache is in use
     bool small_support = false;  // every thread's support count <= cap / 2
+    float f_prev = INFINITY;     // |f| at the previous evaluation
     for (int it = 0;; ++it) {
       // ---- evaluation at tau: m0 = sum z^gamma, m1 = sum z^(gamma-1),
       // m2 = sum z^(gamma-2) over the strict support z > 0, and mc = the size
@@ -350,7 +351,15 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
           lo = fminf(fmaxf(lo, tn), hi);
         }
         const float th = tau - 2.f * f * f1 / (2.f * f1 * f1 - f * f2);  // H_f, Eq. 5
-        tau = (th >= lo - slack && th <= hi + slack) ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
+        bool take = th >= lo - slack && th <= hi + slack;
+        // For gamma < 1 (alpha > 2) f' diverges at every kink x_j, and H_f can
+        // creep towards a kink in ever smaller steps that all stay inside
+        // the bracket, so the fail-safe above never fires.  There the
+        // midpoint is also taken whenever |f| has not halved since the last
+        // evaluation, which bounds the bracket's shrinkage from below.
+        if (!newton_bound && fabsf(f) > 0.5f * f_prev) take = false;
+        f_prev = fabsf(f);
+        tau = take ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
       }
     }
 
