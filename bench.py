@@ -35,6 +35,94 @@ PEAK_BF16_TFLOPS = 2500.0
 KERNELS = ("tau_solve", "compact", "fwd_sparse", "bwd_delta", "bwd_dkdv", "bwd_dq")
 # MFMA block products (64 x 64 x d each) per listed block, by kernel
 PRODUCTS_PER_ACTIVE = {"fwd_sparse": 3, "bwd_dkdv": 4, "bwd_dq": 3}
+# kernel name fragment in profiler output, and the sources that define each kernel
+PROFILE_NAMES = {"tau_solve": "tau_solve_kernel", "fwd_sparse": "fwd_kernel",
+                 "bwd_dkdv": "dkdv_kernel", "bwd_dq": "dq_kernel"}
+KERNEL_SOURCES = {"tau_solve": ["ea_tau.hip"], "fwd_sparse": ["ea_fwd.hip"],
+                  "bwd_dkdv": ["ea_bwd.hip"], "bwd_dq": ["ea_bwd.hip"]}
+COMMON_SOURCES = ["ea_common.h", "ea_internal.h", "../build.py"]
+
+
+def sources_sha256(kernel):
+    """Hash of the files a kernel's code comes from: traffic counters taken on
+    another version of them no longer describe it."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2502_12082_amd", "csrc")
+    for f in KERNEL_SOURCES[kernel] + COMMON_SOURCES:
+        with open(os.path.normpath(os.path.join(csrc, f)), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_path(kernel):
+    return os.path.join(ROOT, "profiles", "traffic_%s.md" % kernel)
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from its committed counter summary, or
+    None when there is none or its sources have changed since."""
+    path = traffic_path(kernel)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if line.startswith("- ") and ": " in line:
+            key, val = line[2:].split(": ", 1)
+            fields[key.strip().strip("`")] = val.strip().strip("`")
+    if fields.get("sources_sha256") != sources_sha256(kernel):
+        return None
+    return float(fields["hbm_bytes_per_launch"])
+
+
+def write_traffic(fetch_csv, write_csv, calib_mib, command):
+    """Scale each kernel's FETCH_SIZE and WRITE_SIZE (KiB per dispatch) by what
+    the same counter reads for the plain copy of `calib_mib` MiB, and write
+    one summary per kernel into profiles/."""
+    import csv
+    import collections
+
+    def per_kernel(path, counter):
+        vals = collections.defaultdict(list)
+        for row in csv.DictReader(open(path)):
+            if row["Counter_Name"] != counter:
+                continue
+            vals[row["Kernel_Name"]].append(float(row["Counter_Value"]))
+        return vals
+
+    fetch = per_kernel(fetch_csv, "FETCH_SIZE")
+    write = per_kernel(write_csv, "WRITE_SIZE")
+    copy_name = [k for k in fetch if "copy" in k.lower()]
+    if not copy_name:
+        raise SystemExit("no copy dispatch in %s (run with --calib-copy-mib)" % fetch_csv)
+    calib_kib = calib_mib * 1024.0
+    cname = max(copy_name, key=lambda k: max(fetch[k]))
+    f_scale = calib_kib / max(fetch[cname])
+    w_scale = calib_kib / max(write[cname])
+    for kernel, frag in PROFILE_NAMES.items():
+        names = [k for k in fetch if frag in k]
+        if not names:
+            continue
+        fk = [v for k in names for v in fetch[k]]
+        wk = [v for k in names for v in write.get(k, [])]
+        f_b = sum(fk) / len(fk) * 1024.0 * f_scale
+        w_b = sum(wk) / len(wk) * 1024.0 * w_scale if wk else 0.0
+        with open(traffic_path(kernel), "w") as fh:
+            fh.write("# HBM traffic of `%s` (rocprofv3 FETCH_SIZE / WRITE_SIZE)\n\n" % frag)
+            fh.write("Commands (repository root on the GPU box; `cd /tmp && export TMPDIR=/tmp` "
+                     "first, one counter per run):\n\n```\n%s\n```\n\n" % command)
+            fh.write("Scaling: the plain device copy of %d MiB read %.0f KiB (FETCH_SIZE) and "
+                     "wrote %.0f KiB (WRITE_SIZE); each counter is multiplied by the ratio of "
+                     "the known size to its copy reading (%.4f, %.4f).\n\n"
+                     % (calib_mib, max(fetch[cname]), max(write[cname]), f_scale, w_scale))
+            fh.write("| dispatches | FETCH_SIZE KiB (mean) | WRITE_SIZE KiB (mean) |\n|---|---|---|\n")
+            fh.write("| %d | %.0f | %.0f |\n\n" % (len(fk), sum(fk) / len(fk),
+                                                      sum(wk) / len(wk) if wk else 0.0))
+            fh.write("- hbm_read_bytes_per_launch: %.0f\n" % f_b)
+            fh.write("- hbm_write_bytes_per_launch: %.0f\n" % w_b)
+            fh.write("- hbm_bytes_per_launch: %.0f\n" % (f_b + w_b))
+            fh.write("- sources_sha256: `%s`\n" % sources_sha256(kernel))
+        print("wrote %s: %.3f GB per launch" % (traffic_path(kernel), (f_b + w_b) / 1e9))
 
 
 def parse():
@@ -54,6 +142,12 @@ def parse():
     ap.add_argument("--causal", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=4, help="heads in the oracle sample")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the timed region, one plain device copy of this many MiB "
+                         "(the reference dispatch for HBM counter scaling)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic_<kernel>.md from two rocprofv3 --pmc runs "
+                         "(FETCH_SIZE, WRITE_SIZE) of this script with --calib-copy-mib, then exit")
     return ap.parse_args()
 
 
@@ -191,6 +285,19 @@ def cpu_baseline(runner, heads):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        mib = args.calib_copy_mib or 1024
+        write_traffic(args.traffic_from[0], args.traffic_from[1], mib,
+                      "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run "
+                      "-- python bench.py --steps 2 --warmup 1 --sweep= --no-cpu-baseline "
+                      "--calib-copy-mib %d\n"
+                      "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run "
+                      "-- python bench.py --steps 2 --warmup 1 --sweep= --no-cpu-baseline "
+                      "--calib-copy-mib %d\n"
+                      "python bench.py --traffic-from gpurun_out/pmc_fetch/run_counter_collection.csv "
+                      "gpurun_out/pmc_write/run_counter_collection.csv --calib-copy-mib %d"
+                      % (mib, mib, mib))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the alpha-entmax path here is a single-GPU "
               "build (heads would shard across GPUs with no communication); --gpus %d is not "
@@ -213,9 +320,18 @@ def main():
                          "tflops": round(work["flops"][name] / (t * 1e-3) / 1e12, 2) if t > 0 else 0.0}
     dom = max(("tau_solve", "fwd_sparse", "bwd_dkdv", "bwd_dq"), key=lambda k_: kern[k_])
     ach = work["flops"][dom] / (kern[dom] * 1e-3) / 1e12
+    traffic = measured_traffic(dom)
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                "traffic": None}
+                "traffic": round(traffic) if traffic is not None else None,
+                "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                                "copy-calibrated)"}
+    if args.calib_copy_mib > 0:
+        src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     out = {
         "metric": METRIC, "value": round(dense_tflops, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
