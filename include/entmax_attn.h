@@ -153,6 +153,31 @@ ea_status entmax_attn_bwd_stage(int stage, const ea_shape* shape, const ea_param
                                 const ea_residuals* res, float* dq, float* dk, float* dv,
                                 void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * Row-wise alpha-entmax of a materialized score matrix s, [rows, n] row-major
+ * in `dtype` (Sec. 3.1): per row, x = (alpha-1) * scale * s, tau from the
+ * hybrid Halley-bisection iteration of Algorithm 1 (Eq. 3-7; the same update
+ * rules, max_iter, tol and early exit as the attention solver), and
+ * p_j = [x_j - tau]_+^(1/(alpha-1)) (Eq. 2).
+ *   params  alpha, scale, max_iter, tol are used; causal and need_bwd are not
+ *   p       fp32 [rows, n] (written), tau fp32 [rows] (written)
+ * 1 <= n <= 32768 (longer rows return EA_ERR_UNSUPPORTED), rows >= 1.  All
+ * pointers are device pointers, 16-byte aligned.  One kernel launch on
+ * `stream`; nothing is allocated.
+ */
+ea_status entmax_rows_fwd(int64_t rows, int32_t n, ea_dtype dtype, const ea_params* params,
+                          const void* s, float* p, float* tau, void* stream);
+
+/*
+ * Backward of entmax_rows_fwd: ds = scale * u * (dp - <u, dp> / sum(u)) per
+ * row, u_j = [x_j - tau]_+^(1/(alpha-1) - 1) on the support (the Jacobian
+ * Diag(u) - u u^T / |u|_1 of Sec. 3.2.2).  s and tau as given to / returned
+ * by the forward; dp, ds fp32 [rows, n].  Same argument rules.
+ */
+ea_status entmax_rows_bwd(int64_t rows, int32_t n, ea_dtype dtype, const ea_params* params,
+                          const void* s, const float* tau, const float* dp, float* ds,
+                          void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* entmax_attn_status_string(ea_status s);
 

@@ -50,6 +50,7 @@ def _load():
         lib.eo_entmax_row.argtypes = [D, i, d, D]
         lib.eo_entmax_row.restype = d
         lib.eo_halley_bisection_trace.argtypes = [D, i, d, i, D]
+        lib.eo_entmax_row_bwd.argtypes = [D, i, d, d, D, D]
         lib.eo_tau.argtypes = [i, i, D, D, d, d, i, I, i, D, i]
         lib.eo_forward_rows.argtypes = [i, i, D, D, D, d, d, i, D, I, i, D, D, i]
         lib.eo_block_margin.argtypes = [i, i, D, D, d, d, i, D, I, i, D, i]
@@ -57,7 +58,7 @@ def _load():
         lib.eo_dq_rows.argtypes = [i, i, D, D, D, D, d, d, i, D, D, I, i, D, i]
         lib.eo_dkdv_cols.argtypes = [i, i, D, D, D, D, d, d, i, D, D, I, i, D, D, i]
         for f in ("eo_halley_bisection_trace", "eo_tau", "eo_forward_rows", "eo_block_margin",
-                  "eo_delta_rows", "eo_dq_rows", "eo_dkdv_cols"):
+                  "eo_delta_rows", "eo_dq_rows", "eo_dkdv_cols", "eo_entmax_row_bwd"):
             getattr(lib, f).restype = None
         _lib = lib
     return _lib
@@ -106,6 +107,14 @@ def entmax(x, alpha: float):
     p = np.empty_like(x)
     tau = _load().eo_entmax_row(_dp(x), x.size, float(alpha), _dp(p))
     return p, tau
+
+
+def entmax_bwd(x, alpha: float, tau: float, g):
+    """Gradient of <g, p> with respect to x / (alpha-1) for p = entmax(x) (one row)."""
+    x, g = _f64(x), _f64(g)
+    out = np.empty_like(x)
+    _load().eo_entmax_row_bwd(_dp(x), x.size, float(alpha), float(tau), _dp(g), _dp(out))
+    return out
 
 
 def halley_bisection_trace(x, alpha: float, iters: int):

@@ -122,6 +122,29 @@ double eo_entmax_row(const double* x, int n, double alpha, double* p) {
 }
 
 /*
+ * Gradient of sum_j g_j p_j with respect to x / (alpha-1) for one row, where
+ * p = alpha-entmax(x) with threshold tau (Sec. 3.2.2): with u_j = [x_j -
+ * tau]_+^(gamma-1) on the strict support z > 0 (0 elsewhere), the Jacobian is
+ * Diag(u) - u u^T / sum(u), so out_j = u_j (g_j - <u, g> / sum(u)).  The
+ * (alpha-1) of the input scaling cancels gamma's factor, as in the attention
+ * backward.
+ */
+void eo_entmax_row_bwd(const double* x, int n, double alpha, double tau, const double* g,
+                       double* out) {
+    const double gamma = 1.0 / (alpha - 1.0);
+    eo_acc su = {0.0, 0.0}, sug = {0.0, 0.0};
+    for (int j = 0; j < n; ++j) {
+        const double z = x[j] - tau;
+        const double u = z > 0.0 ? pow(z, gamma - 1.0) : 0.0;
+        out[j] = u;
+        acc_add(&su, u);
+        acc_add(&sug, u * g[j]);
+    }
+    const double mean = acc_value(&su) > 0.0 ? acc_value(&sug) / acc_value(&su) : 0.0;
+    for (int j = 0; j < n; ++j) out[j] = out[j] * (g[j] - mean);
+}
+
+/*
  * Algorithm 1 (Halley-bisection) run in fp64 on one row x in Eq. 2
  * coordinates, for the iterations-versus-error diagnostic.  Writes the tau
  * held before each of the T updates and after the last one (T+1 values) into

@@ -33,7 +33,8 @@ EA_OK, EA_ERR_INVALID_ARG, EA_ERR_UNSUPPORTED, EA_ERR_WORKSPACE, EA_ERR_HIP = ra
 EA_BF16, EA_F32 = 0, 1
 SYMBOLS = ("entmax_attn_default_params", "entmax_attn_sizes", "entmax_attn_fwd",
            "entmax_attn_bwd", "entmax_attn_fwd_stage", "entmax_attn_bwd_stage",
-           "entmax_attn_status_string", "entmax_attn_last_hip_error")
+           "entmax_attn_status_string", "entmax_attn_last_hip_error", "entmax_rows_fwd",
+           "entmax_rows_bwd")
 
 
 class Shape(ctypes.Structure):
@@ -79,6 +80,12 @@ _lib.entmax_attn_bwd_stage.argtypes = [ctypes.c_int, _P(Shape), _P(Params), _v, 
 _lib.entmax_attn_bwd_stage.restype = ctypes.c_int
 _lib.entmax_attn_status_string.argtypes = [ctypes.c_int]
 _lib.entmax_attn_status_string.restype = ctypes.c_char_p
+_lib.entmax_rows_fwd.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int, _P(Params), _v, _v,
+                                 _v, _v]
+_lib.entmax_rows_fwd.restype = ctypes.c_int
+_lib.entmax_rows_bwd.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int, _P(Params), _v, _v,
+                                 _v, _v, _v]
+_lib.entmax_rows_bwd.restype = ctypes.c_int
 _lib.entmax_attn_last_hip_error.argtypes = []
 _lib.entmax_attn_last_hip_error.restype = ctypes.c_char_p
 
@@ -245,3 +252,52 @@ def backward(q, k, v, dout, res: Residuals, dq=None, dk=None, dv=None, workspace
                            workspace.data_ptr(), workspace.numel() * 4, _stream_handle(q.device)),
            "entmax_attn_bwd")
     return dq, dk, dv
+
+
+# ------------------------------------------------------- row-wise entmax
+
+def entmax_rows_fwd(rows, n, dtype, params, s, p, tau, stream):
+    return _lib.entmax_rows_fwd(rows, n, dtype, ctypes.byref(params), s, p, tau, stream)
+
+
+def entmax_rows_bwd(rows, n, dtype, params, s, tau, dp, ds, stream):
+    return _lib.entmax_rows_bwd(rows, n, dtype, ctypes.byref(params), s, tau, dp, ds, stream)
+
+
+def _row_params(alpha, scale, max_iter, tol):
+    p = default_params()
+    p.alpha, p.scale, p.causal, p.need_bwd = float(alpha), float(scale), 0, 0
+    if max_iter is not None:
+        p.max_iter = int(max_iter)
+    if tol is not None:
+        p.tol = float(tol)
+    return p
+
+
+def rows_forward(s, alpha=1.5, scale=1.0, max_iter=None, tol=None):
+    """(p, tau): alpha-entmax of each row of s ([..., n] bf16/fp32 device tensor)."""
+    if not s.is_cuda or not s.is_contiguous() or s.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("s must be a contiguous bf16 or fp32 device tensor")
+    n = s.shape[-1]
+    rows = s.numel() // n
+    p = torch.empty(s.shape, dtype=torch.float32, device=s.device)
+    tau = torch.empty(s.shape[:-1], dtype=torch.float32, device=s.device)
+    params = _row_params(alpha, scale, max_iter, tol)
+    _check(entmax_rows_fwd(rows, n, EA_BF16 if s.dtype == torch.bfloat16 else EA_F32, params,
+                           s.data_ptr(), p.data_ptr(), tau.data_ptr(), _stream_handle(s.device)),
+           "entmax_rows_fwd")
+    return p, tau
+
+
+def rows_backward(s, tau, dp, alpha=1.5, scale=1.0):
+    """Gradient of sum(dp * p) with respect to s, for (p, tau) = rows_forward(s)."""
+    n = s.shape[-1]
+    rows = s.numel() // n
+    if dp.shape != s.shape or dp.dtype != torch.float32 or not dp.is_contiguous():
+        raise ValueError("dp must be a contiguous fp32 tensor shaped like s")
+    ds = torch.empty(s.shape, dtype=torch.float32, device=s.device)
+    params = _row_params(alpha, scale, None, None)
+    _check(entmax_rows_bwd(rows, n, EA_BF16 if s.dtype == torch.bfloat16 else EA_F32, params,
+                           s.data_ptr(), tau.data_ptr(), dp.data_ptr(), ds.data_ptr(),
+                           _stream_handle(s.device)), "entmax_rows_bwd")
+    return ds

@@ -33,18 +33,24 @@ struct Dims {
   size_t esize;
 };
 
-ea_status check_shape(const ea_shape* s, const ea_params* p, Dims* out) {
-  if (!s || !p) return EA_ERR_INVALID_ARG;
-  if (s->batch < 1 || s->heads < 1 || s->seqlen < 1 || s->head_dim < 1) return EA_ERR_INVALID_ARG;
-  if (s->dtype != EA_BF16 && s->dtype != EA_F32) return EA_ERR_UNSUPPORTED;
-  if (s->head_dim != 64 && s->head_dim != 128) return EA_ERR_UNSUPPORTED;
-  if (s->seqlen > MAX_SEQLEN) return EA_ERR_UNSUPPORTED;
+ea_status check_params(const ea_params* p) {
   if (!std::isfinite(p->alpha) || !(p->alpha > 1.0f)) return EA_ERR_INVALID_ARG;
   if (!std::isfinite(p->scale) || !(p->scale > 0.0f)) return EA_ERR_INVALID_ARG;
   if (p->causal != 0 && p->causal != 1) return EA_ERR_INVALID_ARG;
   if (p->need_bwd != 0 && p->need_bwd != 1) return EA_ERR_INVALID_ARG;
   if (p->max_iter < 0 || p->max_iter > MAX_ITER_CAP) return EA_ERR_INVALID_ARG;
   if (!std::isfinite(p->tol) || p->tol < 0.0f) return EA_ERR_INVALID_ARG;
+  return EA_OK;
+}
+
+ea_status check_shape(const ea_shape* s, const ea_params* p, Dims* out) {
+  if (!s || !p) return EA_ERR_INVALID_ARG;
+  if (s->batch < 1 || s->heads < 1 || s->seqlen < 1 || s->head_dim < 1) return EA_ERR_INVALID_ARG;
+  if (s->dtype != EA_BF16 && s->dtype != EA_F32) return EA_ERR_UNSUPPORTED;
+  if (s->head_dim != 64 && s->head_dim != 128) return EA_ERR_UNSUPPORTED;
+  if (s->seqlen > MAX_SEQLEN) return EA_ERR_UNSUPPORTED;
+  const ea_status st = check_params(p);
+  if (st != EA_OK) return st;
   const int64_t BH = (int64_t)s->batch * s->heads;
   const int64_t n = s->seqlen;
   const int64_t T = (n + 63) / 64;
@@ -93,6 +99,30 @@ ea_status check_tables(const ea_residuals* r) {
 
 // HIP error behind the calling thread's most recent EA_ERR_HIP.
 thread_local hipError_t last_hip_error = hipSuccess;
+
+// Checks shared by the row-wise entry points; fills the kernel arguments.
+ea_status prep_rows(int64_t rows, int32_t n, ea_dtype dtype, const ea_params* params,
+                    const void* s, RowsArgs* ra) {
+  if (!params) return EA_ERR_INVALID_ARG;
+  ea_status st = check_params(params);
+  if (st != EA_OK) return st;
+  if (rows < 1 || n < 1) return EA_ERR_INVALID_ARG;
+  if (dtype != EA_BF16 && dtype != EA_F32) return EA_ERR_UNSUPPORTED;
+  if (n > MAX_ROW_LEN || rows > (int64_t)INT32_MAX) return EA_ERR_UNSUPPORTED;
+  if (!tensor_ok(s)) return EA_ERR_INVALID_ARG;
+  *ra = RowsArgs{};
+  ra->s = s;
+  ra->rows = rows;
+  ra->n = n;
+  ra->alpha = params->alpha;
+  ra->gamma = 1.0f / (params->alpha - 1.0f);
+  ra->scale = params->scale;
+  ra->c = (params->alpha - 1.0f) * params->scale;
+  ra->tol = params->tol;
+  ra->max_iter = params->max_iter;
+  ra->gk = gamma_kind(params->alpha);
+  return EA_OK;
+}
 
 ea_status from_hip(hipError_t e) {
   if (e == hipSuccess) return EA_OK;
@@ -252,6 +282,30 @@ ea_status entmax_attn_bwd_stage(int stage, const ea_shape* shape, const ea_param
   if (st != EA_OK) return st;
   return run_bwd_stage(stage, d, params, q, k, v, dout, res, dq, dk, dv, workspace,
                        static_cast<hipStream_t>(stream));
+}
+
+ea_status entmax_rows_fwd(int64_t rows, int32_t n, ea_dtype dtype, const ea_params* params,
+                          const void* s, float* p, float* tau, void* stream) {
+  RowsArgs ra;
+  ea_status st = prep_rows(rows, n, dtype, params, s, &ra);
+  if (st != EA_OK) return st;
+  if (!tensor_ok(p) || !tensor_ok(tau)) return EA_ERR_INVALID_ARG;
+  ra.p = p;
+  ra.tau = tau;
+  return from_hip(launch_rows_fwd(ra, dtype, static_cast<hipStream_t>(stream)));
+}
+
+ea_status entmax_rows_bwd(int64_t rows, int32_t n, ea_dtype dtype, const ea_params* params,
+                          const void* s, const float* tau, const float* dp, float* ds,
+                          void* stream) {
+  RowsArgs ra;
+  ea_status st = prep_rows(rows, n, dtype, params, s, &ra);
+  if (st != EA_OK) return st;
+  if (!tensor_ok(tau) || !tensor_ok(dp) || !tensor_ok(ds)) return EA_ERR_INVALID_ARG;
+  ra.tau = const_cast<float*>(tau);  // read only by the backward kernel
+  ra.dp = dp;
+  ra.ds = ds;
+  return from_hip(launch_rows_bwd(ra, dtype, static_cast<hipStream_t>(stream)));
 }
 
 const char* entmax_attn_status_string(ea_status s) {

@@ -90,6 +90,23 @@ struct DeltaArgs {
   int64_t rows;
 };
 
+// Row-wise alpha-entmax of a materialized [rows, n] score matrix.
+struct RowsArgs {
+  const void* s;      // [rows, n] scores, input dtype
+  float* p;           // [rows, n] probabilities (forward output)
+  float* tau;         // [rows] thresholds (forward output, backward input)
+  const float* dp;    // [rows, n] gradient of p (backward input)
+  float* ds;          // [rows, n] gradient of s (backward output)
+  int64_t rows;
+  int n;
+  float c;            // (alpha - 1) * scale
+  float alpha, gamma, scale, tol;
+  int max_iter, gk;
+};
+
+// Largest row the row-wise kernels hold in registers.
+constexpr int MAX_ROW_LEN = 32768;
+
 // Each launcher picks the instantiation for (dtype: 0 bf16 / 1 fp32, head_dim,
 // gamma kind) and returns the launch status.
 // Launches `kernel` with its one argument struct and returns the launch's own
@@ -106,5 +123,7 @@ hipError_t launch_fwd(const FwdArgs& a, int dtype, int head_dim, bool train, hip
 hipError_t launch_delta(const DeltaArgs& a, int dtype, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dkdv(const BwdArgs& a, int dtype, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dq(const BwdArgs& a, int dtype, int head_dim, hipStream_t s);
+hipError_t launch_rows_fwd(const RowsArgs& a, int dtype, hipStream_t s);
+hipError_t launch_rows_bwd(const RowsArgs& a, int dtype, hipStream_t s);
 
 }  // namespace ea

@@ -1,0 +1,235 @@
+// ea_rows.hip -- row-wise alpha-entmax of a materialized score matrix.
+//
+// Forward (Sec. 3.1, Algorithm 1): for each row s of length n,
+// x = (alpha-1) * scale * s, tau is the root of f(tau) = sum_j [x_j -
+// tau]_+^gamma - 1 (Eq. 3) found by the hybrid Halley-bisection iteration
+// (Eq. 4, 5, with f', f'' of Eq. 6, 7), and p_j = [x_j - tau]_+^gamma (Eq. 2).
+// Backward: with u_j = [x_j - tau]_+^(gamma-1) on the support, the Jacobian
+// of p with respect to s is scale * (Diag(u) - u u^T / sum u) (Sec. 3.2.2;
+// (alpha-1) gamma = 1), so ds = scale * u (dp - <u, dp> / sum u).
+//
+// Layout: one workgroup of 256 threads per row; thread t keeps elements
+// t + 256 v, v < VPT, in registers, so the row is read once and every
+// evaluation of the iteration runs from registers, with one workgroup
+// reduction per evaluation.  The update rules are those of the attention
+// solver: the bracket test with its rounding slack, the Newton lower bound
+// for gamma >= 1 and the midpoint safeguard for gamma < 1.
+#include "ea_common.h"
+#include "ea_internal.h"
+
+namespace ea {
+
+namespace {
+
+constexpr int ROW_NT = 256;
+
+struct Sums {
+  float a, b, c;
+  int k;
+};
+
+// Workgroup totals of (a, b, c, k); every thread receives them.  The order
+// of the additions is fixed, so results are deterministic.
+__device__ __forceinline__ Sums wg_sum(Sums v, float* sh) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    v.a += __shfl_xor(v.a, o);
+    v.b += __shfl_xor(v.b, o);
+    v.c += __shfl_xor(v.c, o);
+    v.k += __shfl_xor(v.k, o);
+  }
+  const int w = wave_id();
+  if (lane_id() == 0) {
+    sh[4 * w + 0] = v.a;
+    sh[4 * w + 1] = v.b;
+    sh[4 * w + 2] = v.c;
+    sh[4 * w + 3] = __int_as_float(v.k);
+  }
+  __syncthreads();
+  Sums t{0.f, 0.f, 0.f, 0};
+#pragma unroll
+  for (int i = 0; i < ROW_NT / 64; ++i) {
+    t.a += sh[4 * i + 0];
+    t.b += sh[4 * i + 1];
+    t.c += sh[4 * i + 2];
+    t.k += __float_as_int(sh[4 * i + 3]);
+  }
+  __syncthreads();  // sh is reused by the next reduction
+  return t;
+}
+
+__device__ __forceinline__ float wg_max(float v, float* sh) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  if (lane_id() == 0) sh[wave_id()] = v;
+  __syncthreads();
+  float t = sh[0];
+#pragma unroll
+  for (int i = 1; i < ROW_NT / 64; ++i) t = fmaxf(t, sh[i]);
+  __syncthreads();
+  return t;
+}
+
+template <typename E, int VPT>
+__device__ __forceinline__ void load_row(const E* s, int n, float c, float (&x)[VPT]) {
+#pragma unroll
+  for (int v = 0; v < VPT; ++v) {
+    const int j = (int)threadIdx.x + ROW_NT * v;
+    x[v] = j < n ? c * (float)s[j] : -INFINITY;  // padding: [x - tau]_+ = 0
+  }
+}
+
+template <typename E, int VPT, int GK>
+__global__ __launch_bounds__(ROW_NT) void rows_fwd_kernel(RowsArgs a) {
+  __shared__ float sh[4 * (ROW_NT / 64)];
+  const size_t row = blockIdx.x;
+  const int n = a.n;
+  const float c = a.c, g = a.gamma;
+  float x[VPT];
+  load_row<E, VPT>(static_cast<const E*>(a.s) + row * n, n, c, x);
+
+  float mx = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < VPT; ++v) mx = fmaxf(mx, x[v]);
+  const float m = wg_max(mx, sh);
+
+  // Algorithm 1: bracket [m - 1, m - n^(1-alpha)], first tau at its midpoint
+  float lo = m - 1.f, hi = m - powf((float)n, 1.f - a.alpha);
+  float tau = 0.5f * (lo + hi);
+  const bool newton_bound = g >= 1.f;
+  float f_prev = INFINITY;
+  for (int it = 0;; ++it) {
+    Sums t{0.f, 0.f, 0.f, 0};
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) {
+      const float zp = __builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f);
+      if constexpr (GK == 1) {
+        t.a += zp;
+        t.k += in_support(zp);
+      } else if constexpr (GK == 2) {
+        t.a = fmaf(zp, zp, t.a);
+        t.b += zp;
+        t.k += in_support(zp);
+      } else if constexpr (GK == 4) {
+        const float z2 = zp * zp;
+        t.a = fmaf(z2, z2, t.a);
+        t.b = fmaf(z2, zp, t.b);
+        t.c += z2;
+      } else {
+        if (zp > 0.f) {
+          const float l = __log2f(zp);
+          t.a += exp2f(g * l);
+          t.b += exp2f((g - 1.f) * l);
+          t.c += exp2f((g - 2.f) * l);
+        }
+      }
+    }
+    const Sums tot = wg_sum(t, sh);
+    const float f = tot.a - 1.f;  // Eq. 3
+    float f1, f2;                 // Eq. 6, 7
+    if constexpr (GK == 1) {
+      f1 = -(float)tot.k;
+      f2 = 0.f;
+    } else if constexpr (GK == 2) {
+      f1 = -2.f * tot.b;
+      f2 = 2.f * (float)tot.k;
+    } else if constexpr (GK == 4) {
+      f1 = -4.f * tot.b;
+      f2 = 12.f * tot.c;
+    } else {
+      f1 = -g * tot.b;
+      f2 = g * (g - 1.f) * tot.c;
+    }
+    if (fabsf(f) <= a.tol || it >= a.max_iter) break;
+    if (f < 0.f)  // B_f, Eq. 4
+      hi = tau;
+    else
+      lo = tau;
+    const float slack = 1e-6f * fmaxf(1.f, fmaxf(fabsf(lo), fabsf(hi)));
+    if (newton_bound && f1 < 0.f) lo = fminf(fmaxf(lo, tau - f / f1 - 10.f * slack), hi);
+    const float th = tau - 2.f * f * f1 / (2.f * f1 * f1 - f * f2);  // H_f, Eq. 5
+    bool take = th >= lo - slack && th <= hi + slack;
+    if (!newton_bound && fabsf(f) > 0.5f * f_prev) take = false;
+    f_prev = fabsf(f);
+    tau = take ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
+  }
+
+  float* p = a.p + row * n;
+#pragma unroll
+  for (int v = 0; v < VPT; ++v) {
+    const int j = (int)threadIdx.x + ROW_NT * v;
+    if (j < n) p[j] = Gamma<GK>::p_only(__builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f), g);
+  }
+  if (threadIdx.x == 0) a.tau[row] = tau;
+}
+
+template <typename E, int VPT, int GK>
+__global__ __launch_bounds__(ROW_NT) void rows_bwd_kernel(RowsArgs a) {
+  __shared__ float sh[4 * (ROW_NT / 64)];
+  const size_t row = blockIdx.x;
+  const int n = a.n;
+  const float c = a.c, g = a.gamma;
+  const float tau = a.tau[row];
+  float x[VPT];
+  load_row<E, VPT>(static_cast<const E*>(a.s) + row * n, n, c, x);
+  const float* dp = a.dp + row * n;
+  float u[VPT], gv[VPT];
+  Sums t{0.f, 0.f, 0.f, 0};
+#pragma unroll
+  for (int v = 0; v < VPT; ++v) {
+    const int j = (int)threadIdx.x + ROW_NT * v;
+    float p;
+    Gamma<GK>::pu(__builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f), g, p, u[v]);
+    gv[v] = j < n ? dp[j] : 0.f;
+    t.a += u[v];
+    t.b = fmaf(u[v], gv[v], t.b);
+  }
+  const Sums tot = wg_sum(t, sh);
+  const float mean = tot.a > 0.f ? tot.b / tot.a : 0.f;  // <u, dp> / sum u
+  float* ds = a.ds + row * n;
+#pragma unroll
+  for (int v = 0; v < VPT; ++v) {
+    const int j = (int)threadIdx.x + ROW_NT * v;
+    if (j < n) ds[j] = a.scale * u[v] * (gv[v] - mean);
+  }
+}
+
+template <typename E, int VPT, bool BWD>
+hipError_t launch_rows_v(const RowsArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)a.rows), block(ROW_NT);
+  if constexpr (BWD) {
+    auto kernel = rows_bwd_kernel<E, VPT, 0>;
+    if (a.gk == 1) kernel = rows_bwd_kernel<E, VPT, 1>;
+    if (a.gk == 2) kernel = rows_bwd_kernel<E, VPT, 2>;
+    if (a.gk == 4) kernel = rows_bwd_kernel<E, VPT, 4>;
+    return launch_kernel(kernel, grid, block, s, a);
+  } else {
+    auto kernel = rows_fwd_kernel<E, VPT, 0>;
+    if (a.gk == 1) kernel = rows_fwd_kernel<E, VPT, 1>;
+    if (a.gk == 2) kernel = rows_fwd_kernel<E, VPT, 2>;
+    if (a.gk == 4) kernel = rows_fwd_kernel<E, VPT, 4>;
+    return launch_kernel(kernel, grid, block, s, a);
+  }
+}
+
+// The smallest register row that holds n elements.
+template <typename E, bool BWD>
+hipError_t launch_rows_e(const RowsArgs& a, hipStream_t s) {
+  if (a.n <= ROW_NT * 4) return launch_rows_v<E, 4, BWD>(a, s);
+  if (a.n <= ROW_NT * 16) return launch_rows_v<E, 16, BWD>(a, s);
+  if (a.n <= ROW_NT * 32) return launch_rows_v<E, 32, BWD>(a, s);
+  if (a.n <= ROW_NT * 64) return launch_rows_v<E, 64, BWD>(a, s);
+  return launch_rows_v<E, 128, BWD>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_rows_fwd(const RowsArgs& a, int dtype, hipStream_t s) {
+  return dtype == 0 ? launch_rows_e<__bf16, false>(a, s) : launch_rows_e<float, false>(a, s);
+}
+
+hipError_t launch_rows_bwd(const RowsArgs& a, int dtype, hipStream_t s) {
+  return dtype == 0 ? launch_rows_e<__bf16, true>(a, s) : launch_rows_e<float, true>(a, s);
+}
+
+}  // namespace ea

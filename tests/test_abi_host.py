@@ -17,7 +17,7 @@ ea = pytest.importorskip("paper_2502_12082_amd", reason="HIP library not built")
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(entmax_attn_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(entmax_\w+)\s*\(", text)))
 
 
 def test_exports_every_declared_symbol():
@@ -151,3 +151,20 @@ def test_single_hip_runtime_after_import():
                          text=True, timeout=300)
     assert out.returncode == 0, out.stderr
     assert out.stdout.strip().splitlines()[-1] == "1"
+
+
+def test_rows_validation():
+    p = ea.default_params()
+    f = ea.entmax_rows_fwd
+    assert f(4, 100, ea.EA_F32, p, None, _fake(), _fake(), None) == ea.EA_ERR_INVALID_ARG
+    assert f(0, 100, ea.EA_F32, p, _fake(), _fake(), _fake(), None) == ea.EA_ERR_INVALID_ARG
+    assert f(4, 0, ea.EA_F32, p, _fake(), _fake(), _fake(), None) == ea.EA_ERR_INVALID_ARG
+    assert f(4, 32769, ea.EA_F32, p, _fake(), _fake(), _fake(), None) == ea.EA_ERR_UNSUPPORTED
+    assert f(4, 100, 5, p, _fake(), _fake(), _fake(), None) == ea.EA_ERR_UNSUPPORTED
+    assert f(4, 100, ea.EA_F32, p, _fake(), _fake() + 4, _fake(), None) == ea.EA_ERR_INVALID_ARG
+    p.alpha = 0.9
+    assert f(4, 100, ea.EA_F32, p, _fake(), _fake(), _fake(), None) == ea.EA_ERR_INVALID_ARG
+    p = ea.default_params()
+    b = ea.entmax_rows_bwd
+    assert b(4, 100, ea.EA_BF16, p, _fake(), _fake(), None, _fake(), None) == ea.EA_ERR_INVALID_ARG
+    assert b(4, 100, ea.EA_BF16, p, _fake(), _fake(), _fake(), None, None) == ea.EA_ERR_INVALID_ARG

@@ -283,3 +283,29 @@ def test_backward_row_sum_invariants():
         U = np.where(z > 0, z, 0.0)
         dP = do @ v.T
         assert np.max(np.abs((U * dP).sum(1) / U.sum(1) - out["delta"])) < 1e-11
+
+
+@pytest.mark.parametrize("alpha", [1.25, 1.5, 2.0, 3.0])
+def test_row_backward_finite_differences(alpha):
+    """The row-wise backward (gradient of <g, p> with respect to s, where
+    x = (alpha-1) s) against central differences of the oracle's forward."""
+    rng = np.random.default_rng(int(alpha * 100))
+    n, h = 12, 1e-7
+    for _ in range(50):  # a seed whose scores sit away from the support edge
+        s = rng.standard_normal(n) * 3
+        x = (alpha - 1) * s
+        tau = oracle.entmax_threshold(x, alpha)
+        if np.min(np.abs(x - tau)) > 1e-3:
+            break
+    g = rng.standard_normal(n)
+    grad = oracle.entmax_bwd(x, alpha, tau, g)
+    fd = np.zeros(n)
+    for j in range(n):
+        sp, sm = s.copy(), s.copy()
+        sp[j] += h
+        sm[j] -= h
+        fd[j] = (g @ oracle.entmax((alpha - 1) * sp, alpha)[0]
+                 - g @ oracle.entmax((alpha - 1) * sm, alpha)[0]) / (2 * h)
+    assert np.max(np.abs(fd - grad)) <= 1e-6 * max(1.0, np.max(np.abs(grad)))
+    # the Jacobian annihilates constants: gradients sum to zero over the row
+    assert abs(grad.sum()) <= 1e-12 * max(1.0, np.abs(grad).max()) * n
