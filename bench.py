@@ -142,6 +142,8 @@ def parse():
     ap.add_argument("--causal", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=4, help="heads in the oracle sample")
+    ap.add_argument("--no-rows", action="store_true",
+                    help="skip the row-wise entmax measurement (materialized 8192 x 8192 scores)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed region, one plain device copy of this many MiB "
                          "(the reference dispatch for HBM counter scaling)")
@@ -261,6 +263,43 @@ class Runner:
         return 1.0 - float((x > 0).sum()) / valid
 
 
+PEAK_HBM_GBS = 8000.0
+
+
+def rows_bench(steps=20, warmup=3, rows=8192, n=8192, alpha=1.5):
+    """Row-wise alpha-entmax of a materialized [rows, n] fp32 Gaussian score
+    matrix (the shape of the paper's Halley-bisection efficiency benchmark):
+    forward (p, tau) and backward (ds), each HBM-bound; achieved = bytes one
+    launch must move (read s; write p) or (read s, dp; write ds) / time."""
+    import torch
+    import paper_2502_12082_amd as ea
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(20250217 + 7)
+    s = torch.randn((rows, n), generator=gen, device="cuda", dtype=torch.float32)
+    dp = torch.randn((rows, n), generator=gen, device="cuda", dtype=torch.float32)
+    out = {}
+    for kind in ("fwd", "bwd"):
+        p, tau = ea.rows_forward(s, alpha=alpha)
+        fn = (lambda: ea.rows_forward(s, alpha=alpha)) if kind == "fwd" else \
+            (lambda: ea.rows_backward(s, tau, dp, alpha=alpha))
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / steps
+        nbytes = rows * n * 4 * (2 if kind == "fwd" else 3) + rows * 4
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out[kind] = {"ms": round(ms, 4), "GB/s": round(gbs, 1),
+                     "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+    out["shape"] = "%d x %d fp32, alpha %g, N(0,1) scores" % (rows, n, alpha)
+    return out
+
+
 def cpu_baseline(runner, heads):
     """The oracle (fp64, all host cores) on `heads` heads of the same workload:
     tau, O, O2, block margins, delta, dQ, dK, dV of every row and column."""
@@ -371,6 +410,8 @@ def main():
         torch.cuda.empty_cache()
     if sweep:
         out["sweep"] = sweep
+    if not args.no_rows:
+        out["entmax_rows"] = rows_bench()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(run, args.cpu_heads)
     print(json.dumps(out), flush=True)

@@ -9,7 +9,8 @@
 // (alpha-1) gamma = 1), so ds = scale * u (dp - <u, dp> / sum u).
 //
 // Layout: one workgroup of 256 threads per row; thread t keeps elements
-// t + 256 v, v < VPT, in registers, so the row is read once and every
+// 4 (t + 256 w) + e, w < VPT / 4, e < 4, in registers (16-byte accesses when
+// n is a multiple of 8), so the row is read once and every
 // evaluation of the iteration runs from registers, with one workgroup
 // reduction per evaluation.  The update rules are those of the attention
 // solver: the bracket test with its rounding slack, the Newton lower bound
@@ -70,12 +71,53 @@ __device__ __forceinline__ float wg_max(float v, float* sh) {
   return t;
 }
 
+// Element held in slot v of the calling thread: groups of 4 consecutive
+// elements, so that rows whose length is a multiple of 8 move in 16-byte
+// (fp32) or 8-byte (bf16) accesses.
+template <int VPT>
+__device__ __forceinline__ int row_elem(int v) {
+  return 4 * ((int)threadIdx.x + ROW_NT * (v / 4)) + (v % 4);
+}
+
 template <typename E, int VPT>
 __device__ __forceinline__ void load_row(const E* s, int n, float c, float (&x)[VPT]) {
+  static_assert(VPT % 4 == 0, "slots come in groups of 4");
+  const bool vec = (n % 8) == 0;
 #pragma unroll
-  for (int v = 0; v < VPT; ++v) {
-    const int j = (int)threadIdx.x + ROW_NT * v;
-    x[v] = j < n ? c * (float)s[j] : -INFINITY;  // padding: [x - tau]_+ = 0
+  for (int g4 = 0; g4 < VPT / 4; ++g4) {
+    const int j0 = row_elem<VPT>(4 * g4);
+    if (vec && j0 < n) {
+      if constexpr (sizeof(E) == 4) {
+        const f32x4 v4 = *reinterpret_cast<const f32x4*>(s + j0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * g4 + e] = c * v4[e];
+      } else {
+        const bf16x4 v4 = *reinterpret_cast<const bf16x4*>(s + j0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * g4 + e] = c * (float)v4[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        x[4 * g4 + e] = j0 + e < n ? c * (float)s[j0 + e] : -INFINITY;  // padding: [x - tau]_+ = 0
+    }
+  }
+}
+
+// Stores slot values y to row r (length n) in the same element order.
+template <int VPT>
+__device__ __forceinline__ void store_row(float* r, int n, const float (&y)[VPT]) {
+  const bool vec = (n % 8) == 0;
+#pragma unroll
+  for (int g4 = 0; g4 < VPT / 4; ++g4) {
+    const int j0 = row_elem<VPT>(4 * g4);
+    if (vec && j0 < n) {
+      *reinterpret_cast<f32x4*>(r + j0) = f32x4{y[4 * g4], y[4 * g4 + 1], y[4 * g4 + 2], y[4 * g4 + 3]};
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j0 + e < n) r[j0 + e] = y[4 * g4 + e];
+    }
   }
 }
 
@@ -154,12 +196,10 @@ __global__ __launch_bounds__(ROW_NT) void rows_fwd_kernel(RowsArgs a) {
     tau = take ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
   }
 
-  float* p = a.p + row * n;
+  float pv[VPT];
 #pragma unroll
-  for (int v = 0; v < VPT; ++v) {
-    const int j = (int)threadIdx.x + ROW_NT * v;
-    if (j < n) p[j] = Gamma<GK>::p_only(__builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f), g);
-  }
+  for (int v = 0; v < VPT; ++v) pv[v] = Gamma<GK>::p_only(__builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f), g);
+  store_row<VPT>(a.p + row * n, n, pv);
   if (threadIdx.x == 0) a.tau[row] = tau;
 }
 
@@ -172,26 +212,22 @@ __global__ __launch_bounds__(ROW_NT) void rows_bwd_kernel(RowsArgs a) {
   const float tau = a.tau[row];
   float x[VPT];
   load_row<E, VPT>(static_cast<const E*>(a.s) + row * n, n, c, x);
-  const float* dp = a.dp + row * n;
   float u[VPT], gv[VPT];
+  load_row<float, VPT>(a.dp + row * n, n, 1.f, gv);  // padding reads -inf; its u is 0
   Sums t{0.f, 0.f, 0.f, 0};
 #pragma unroll
   for (int v = 0; v < VPT; ++v) {
-    const int j = (int)threadIdx.x + ROW_NT * v;
     float p;
     Gamma<GK>::pu(__builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f), g, p, u[v]);
-    gv[v] = j < n ? dp[j] : 0.f;
+    if (u[v] == 0.f) gv[v] = 0.f;
     t.a += u[v];
     t.b = fmaf(u[v], gv[v], t.b);
   }
   const Sums tot = wg_sum(t, sh);
   const float mean = tot.a > 0.f ? tot.b / tot.a : 0.f;  // <u, dp> / sum u
-  float* ds = a.ds + row * n;
 #pragma unroll
-  for (int v = 0; v < VPT; ++v) {
-    const int j = (int)threadIdx.x + ROW_NT * v;
-    if (j < n) ds[j] = a.scale * u[v] * (gv[v] - mean);
-  }
+  for (int v = 0; v < VPT; ++v) gv[v] = a.scale * u[v] * (gv[v] - mean);
+  store_row<VPT>(a.ds + row * n, n, gv);
 }
 
 template <typename E, int VPT, bool BWD>
