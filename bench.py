@@ -300,6 +300,35 @@ def rows_bench(steps=20, warmup=3, rows=8192, n=8192, alpha=1.5):
     return out
 
 
+def dense_mode_bench(run, steps=5, warmup=2):
+    """The no-mask mode (fused tau + O forward, table-free backward) on the
+    headline workload: ms per fwd+bwd step and dense-equivalent TFLOP/s."""
+    import torch
+    import paper_2502_12082_amd as ea
+    q, k, v, do = run.q, run.k, run.v, run.do
+    p = run.params
+    kw = dict(alpha=p.alpha, scale=p.scale, causal=bool(p.causal))
+    ws = ea.forward_workspace(run.res, q.device)
+
+    def step():
+        o, tau, o2 = ea.forward_dense(q, k, v, need_bwd=True, workspace=ws, **kw)
+        ea.backward_dense(q, k, v, do, tau, o2, **kw)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        step()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    dense = 14.0 * run.n * run.n * run.d * run.B * run.H * (0.5 if p.causal else 1.0)
+    return {"ms_per_step": round(ms, 4), "tflops_dense_equiv": round(dense / (ms * 1e-3) / 1e12, 3),
+            "note": "includes the binding's buffer allocations (torch caching allocator)"}
+
+
 def cpu_baseline(runner, heads):
     """The oracle (fp64, all host cores) on `heads` heads of the same workload:
     tau, O, O2, block margins, delta, dQ, dK, dV of every row and column."""
@@ -412,6 +441,7 @@ def main():
         out["sweep"] = sweep
     if not args.no_rows:
         out["entmax_rows"] = rows_bench()
+        out["no_mask_mode"] = dense_mode_bench(run)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(run, args.cpu_heads)
     print(json.dumps(out), flush=True)

@@ -154,6 +154,26 @@ ea_status entmax_attn_bwd_stage(int stage, const ea_shape* shape, const ea_param
                                 void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * No-mask ("memory-efficient") mode, Algorithm 2 as written (Sec. 3.2.1): the
+ * forward solves tau and accumulates O (and, if need_bwd, o2) in one kernel
+ * per 128-row query tile, visiting every valid key block; no block mask or
+ * tables exist, so memory beyond the inputs and outputs is O(n) per head.
+ *   tau  fp32 [BH, n] (written); o2 fp32 [BH, n, d] (written if need_bwd)
+ *   workspace  optional candidate cache, as for entmax_attn_fwd
+ * The backward visits every valid block (no tables) and otherwise follows
+ * entmax_attn_bwd: workspace >= sizes.ws_bwd bytes.  Results equal those of
+ * entmax_attn_fwd / entmax_attn_bwd up to rounding.  One kernel launch
+ * (forward) or three (backward) on `stream`.
+ */
+ea_status entmax_attn_fwd_dense(const ea_shape* shape, const ea_params* params, const void* q,
+                                const void* k, const void* v, void* o, float* tau, float* o2,
+                                void* workspace, size_t ws_bytes, void* stream);
+ea_status entmax_attn_bwd_dense(const ea_shape* shape, const ea_params* params, const void* q,
+                                const void* k, const void* v, const void* dout, const float* tau,
+                                const float* o2, float* dq, float* dk, float* dv, void* workspace,
+                                size_t ws_bytes, void* stream);
+
+/*
  * Row-wise alpha-entmax of a materialized score matrix s, [rows, n] row-major
  * in `dtype` (Sec. 3.1): per row, x = (alpha-1) * scale * s, tau from the
  * hybrid Halley-bisection iteration of Algorithm 1 (Eq. 3-7; the same update

@@ -34,7 +34,7 @@ EA_BF16, EA_F32 = 0, 1
 SYMBOLS = ("entmax_attn_default_params", "entmax_attn_sizes", "entmax_attn_fwd",
            "entmax_attn_bwd", "entmax_attn_fwd_stage", "entmax_attn_bwd_stage",
            "entmax_attn_status_string", "entmax_attn_last_hip_error", "entmax_rows_fwd",
-           "entmax_rows_bwd")
+           "entmax_rows_bwd", "entmax_attn_fwd_dense", "entmax_attn_bwd_dense")
 
 
 class Shape(ctypes.Structure):
@@ -80,6 +80,12 @@ _lib.entmax_attn_bwd_stage.argtypes = [ctypes.c_int, _P(Shape), _P(Params), _v, 
 _lib.entmax_attn_bwd_stage.restype = ctypes.c_int
 _lib.entmax_attn_status_string.argtypes = [ctypes.c_int]
 _lib.entmax_attn_status_string.restype = ctypes.c_char_p
+_lib.entmax_attn_fwd_dense.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _v, _v, _v,
+                                       ctypes.c_size_t, _v]
+_lib.entmax_attn_fwd_dense.restype = ctypes.c_int
+_lib.entmax_attn_bwd_dense.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _v, _v, _v, _v, _v,
+                                       _v, ctypes.c_size_t, _v]
+_lib.entmax_attn_bwd_dense.restype = ctypes.c_int
 _lib.entmax_rows_fwd.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int, _P(Params), _v, _v,
                                  _v, _v]
 _lib.entmax_rows_fwd.restype = ctypes.c_int
@@ -301,3 +307,42 @@ def rows_backward(s, tau, dp, alpha=1.5, scale=1.0):
                            s.data_ptr(), tau.data_ptr(), dp.data_ptr(), ds.data_ptr(),
                            _stream_handle(s.device)), "entmax_rows_bwd")
     return ds
+
+
+# ---------------------------------------------------------- no-mask mode
+
+def forward_dense(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_iter=None,
+                  tol=None, workspace=None):
+    """(O, tau, O2 or None) without block mask or tables (Algorithm 2 as written)."""
+    shape = make_shape(q)
+    params = make_params(alpha, scale, causal, need_bwd, max_iter, tol, head_dim=q.shape[-1])
+    B, H, n, d = q.shape
+    o = torch.empty_like(q)
+    tau = torch.empty((B * H, n), dtype=torch.float32, device=q.device)
+    o2 = torch.empty(q.shape, dtype=torch.float32, device=q.device) if need_bwd else None
+    z = entmax_attn_sizes(shape, params)
+    if workspace is None:
+        workspace = torch.empty(max(z.ws_fwd, 16), dtype=torch.uint8, device=q.device)
+    ws_ptr, ws_bytes = (None, 0) if workspace is False else (workspace.data_ptr(),
+                                                            workspace.numel() * workspace.element_size())
+    _check(_lib.entmax_attn_fwd_dense(ctypes.byref(shape), ctypes.byref(params), q.data_ptr(),
+                                      k.data_ptr(), v.data_ptr(), o.data_ptr(), tau.data_ptr(),
+                                      o2.data_ptr() if o2 is not None else None, ws_ptr, ws_bytes,
+                                      _stream_handle(q.device)), "entmax_attn_fwd_dense")
+    return o, tau, o2
+
+
+def backward_dense(q, k, v, dout, tau, o2, alpha=1.5, scale=None, causal=False):
+    """(dQ, dK, dV) in fp32 for the no-mask forward that produced tau and o2."""
+    shape = make_shape(q)
+    params = make_params(alpha, scale, causal, True, None, None, head_dim=q.shape[-1])
+    z = entmax_attn_sizes(shape, params)
+    mk = lambda: torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    dq, dk, dv = mk(), mk(), mk()
+    ws = torch.empty(max(z.ws_bwd, 16) // 4 + 4, dtype=torch.float32, device=q.device)
+    _check(_lib.entmax_attn_bwd_dense(ctypes.byref(shape), ctypes.byref(params), q.data_ptr(),
+                                      k.data_ptr(), v.data_ptr(), dout.data_ptr(), tau.data_ptr(),
+                                      o2.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                      ws.data_ptr(), ws.numel() * 4, _stream_handle(q.device)),
+           "entmax_attn_bwd_dense")
+    return dq, dk, dv

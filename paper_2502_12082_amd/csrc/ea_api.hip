@@ -184,7 +184,8 @@ ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const
     const int64_t most = cache_slots(d);
     if (slots > most) slots = most;
     CandEntry* cand = slots > 0 ? static_cast<CandEntry*>(workspace) : nullptr;
-    TauArgs ta{q, k, res->tau, res->block_mask, res->stats, cand, TAU_CACHE_CAP, (int)slots,
+    TauArgs ta{q, k, res->tau, res->block_mask, res->stats, nullptr, nullptr, nullptr, cand,
+               TAU_CACHE_CAP, (int)slots,
                (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma, params->causal,
                params->max_iter, params->tol, gk};
     return from_hip(launch_tau(ta, d.dtype, (int)d.d, s));
@@ -306,6 +307,50 @@ ea_status entmax_rows_bwd(int64_t rows, int32_t n, ea_dtype dtype, const ea_para
   ra.dp = dp;
   ra.ds = ds;
   return from_hip(launch_rows_bwd(ra, dtype, static_cast<hipStream_t>(stream)));
+}
+
+ea_status entmax_attn_fwd_dense(const ea_shape* shape, const ea_params* params, const void* q,
+                                const void* k, const void* v, void* o, float* tau, float* o2,
+                                void* workspace, size_t ws_bytes, void* stream) {
+  Dims d;
+  ea_status st = check_shape(shape, params, &d);
+  if (st != EA_OK) return st;
+  if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(o)) return EA_ERR_INVALID_ARG;
+  if (!small_ok(tau)) return EA_ERR_INVALID_ARG;
+  if (params->need_bwd && !tensor_ok(o2)) return EA_ERR_INVALID_ARG;
+  if (workspace && !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
+  int64_t slots = workspace ? (int64_t)(ws_bytes / TAU_SLOT_BYTES) : 0;
+  if (slots > cache_slots(d)) slots = cache_slots(d);
+  CandEntry* cand = slots > 0 ? static_cast<CandEntry*>(workspace) : nullptr;
+  const float c = (params->alpha - 1.0f) * params->scale;
+  const float gamma = 1.0f / (params->alpha - 1.0f);
+  TauArgs ta{q, k, tau, nullptr, nullptr, v, o, params->need_bwd ? o2 : nullptr, cand,
+             TAU_CACHE_CAP, (int)slots, (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma,
+             params->causal, params->max_iter, params->tol, gamma_kind(params->alpha)};
+  return from_hip(launch_tau_fused(ta, d.dtype, (int)d.d, static_cast<hipStream_t>(stream)));
+}
+
+ea_status entmax_attn_bwd_dense(const ea_shape* shape, const ea_params* params, const void* q,
+                                const void* k, const void* v, const void* dout, const float* tau,
+                                const float* o2, float* dq, float* dk, float* dv, void* workspace,
+                                size_t ws_bytes, void* stream) {
+  Dims d;
+  ea_status st = check_shape(shape, params, &d);
+  if (st != EA_OK) return st;
+  if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(dout)) return EA_ERR_INVALID_ARG;
+  if (!tensor_ok(dq) || !tensor_ok(dk) || !tensor_ok(dv)) return EA_ERR_INVALID_ARG;
+  if (!small_ok(tau) || !tensor_ok(o2)) return EA_ERR_INVALID_ARG;
+  if (!workspace || !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
+  if (ws_bytes < bwd_ws_bytes(d)) return EA_ERR_WORKSPACE;
+  // no tables: the kernels visit every valid block
+  ea_residuals res{};
+  res.tau = const_cast<float*>(tau);
+  res.o2 = const_cast<float*>(o2);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int stage = 0; stage < 3; ++stage)
+    if ((st = run_bwd_stage(stage, d, params, q, k, v, dout, &res, dq, dk, dv, workspace, s)) != EA_OK)
+      return st;
+  return EA_OK;
 }
 
 const char* entmax_attn_status_string(ea_status s) {

@@ -90,8 +90,11 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
     vf[kk] = load_row_frag_global<E, D>(Vg, j, n, kk);
   }
 
-  const int32_t* list = a.k_index + ((size_t)bh * T + kb) * T;
-  const int cnt = a.k_count[(size_t)bh * T + kb];
+  // Without tables (the no-mask mode) every valid query block is visited.
+  const bool dense = a.k_index == nullptr;
+  const int32_t* list = dense ? nullptr : a.k_index + ((size_t)bh * T + kb) * T;
+  const int cnt = dense ? (a.causal ? T - kb : T) : a.k_count[(size_t)bh * T + kb];
+  auto qb_of = [&](int e) { return dense ? (a.causal ? kb + e : e) : list[e]; };
 
   f32x16 dk[NTD], dv[NTD];
 #pragma unroll
@@ -154,7 +157,7 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
   DmaPlan<E, D, BWD_NT> dma;
   dma.init();
   auto issue = [&](int e) {
-    const int qb = list[e];
+    const int qb = qb_of(e);
     dma.issue(qbuf[e & 1], Qg, qb * BLK, n);
     dma.issue(dobuf[e & 1], dOg, qb * BLK, n);
     if (threadIdx.x < BLK) {
@@ -171,7 +174,7 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
       del_s[e & 1][threadIdx.x] = dlv;
     }
     __syncthreads();
-    const int qb = list[e];
+    const int qb = qb_of(e);
     if (e + 1 < cnt) issue(e + 1);
     if (!wave_ok) continue;
     const E* qt = qbuf[e & 1];
@@ -248,8 +251,11 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
     df[kk] = load_row_frag_global<E, D>(dOg, i, n, kk);
   }
 
-  const int32_t* list = a.q_index + ((size_t)bh * T + qb) * T;
-  const int cnt = a.q_count[(size_t)bh * T + qb];
+  // Without tables (the no-mask mode) every valid key block is visited.
+  const bool dense = a.q_index == nullptr;
+  const int32_t* list = dense ? nullptr : a.q_index + ((size_t)bh * T + qb) * T;
+  const int cnt = dense ? (a.causal ? qb + 1 : T) : a.q_count[(size_t)bh * T + qb];
+  auto kb_of = [&](int e) { return dense ? e : list[e]; };
 
   f32x16 dq[NTD];
 #pragma unroll
@@ -265,7 +271,7 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
   DmaPlan<E, D, DQ_NT> dma;
   dma.init();
   auto issue = [&](int e) {
-    const int kb = list[e];
+    const int kb = kb_of(e);
     dma.issue(kbuf[e & 1], Kg, kb * BLK, n);
     dma.issue(vbuf[e & 1], Vg, kb * BLK, n);
   };
@@ -276,7 +282,7 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
     if (e + 1 < cnt) issue(e + 1);
     const E* kt = kbuf[e & 1];
     const E* vt = vbuf[e & 1];
-    const int j0 = list[e] * BLK + 32 * kh;
+    const int j0 = kb_of(e) * BLK + 32 * kh;
     const int kind = sub_kind(j0);
     if (kind == 0) continue;
     // S^T = K Q^T and dP^T = V dO^T for this wave's 32 keys x 32 queries

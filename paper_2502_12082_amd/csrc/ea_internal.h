@@ -33,6 +33,11 @@ struct TauArgs {
   float* tau;         // [BH, n]
   uint8_t* mask;      // [BH, T, T]
   int32_t* stats;     // [BH, T] K passes run for each 64-row query block, or null
+  // no-mask mode only (mask, stats null): O and, when training, O2 are
+  // accumulated by the solver kernel itself once tau is known
+  const void* v;
+  void* o;            // [BH, n, D] input dtype
+  float* o2;          // [BH, n, D] fp32, or null (inference)
   CandEntry* cand;    // candidate cache: [slots][cap][TAU_THREADS], or null
   int cap;            // entries per thread
   int slots;          // 128-row tiles with a cache slot (tile t uses slot t)
@@ -118,6 +123,8 @@ inline hipError_t launch_kernel(void (*kernel)(A), dim3 grid, dim3 block, hipStr
 }
 
 hipError_t launch_tau(const TauArgs& a, int dtype, int head_dim, hipStream_t s);
+// The no-mask forward: tau, then O (and O2 if a.o2) in the same kernel.
+hipError_t launch_tau_fused(const TauArgs& a, int dtype, int head_dim, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int head_dim, bool train, hipStream_t s);
 hipError_t launch_delta(const DeltaArgs& a, int dtype, int head_dim, hipStream_t s);

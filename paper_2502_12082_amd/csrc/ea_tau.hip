@@ -33,13 +33,24 @@ constexpr int TAU_WAVES = 4;
 constexpr int TAU_NT = 64 * TAU_WAVES;
 constexpr int TAU_ROWS = 32 * TAU_WAVES;
 
-template <typename E, int D, int GK>
-__global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
+// MODE: SOLVE writes tau, the block mask and stats; FUSED_O (inference) and
+// FUSED_O2 (training) are the no-mask forward of Algorithm 2: once tau is
+// known, the same workgroup streams K and V once more and writes O (and
+// O2), with no mask or tables.
+constexpr int SOLVE = 0, FUSED_O = 1, FUSED_O2 = 2;
+
+template <typename E, int D, int GK, int MODE>
+__global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kernel(TauArgs a) {
   using TL = PadTile<E, D>;
+  using TV = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
+  constexpr int NTD = D / 32;
+  constexpr int PS = perm_steps<E>();
+  constexpr bool FUSED = MODE != SOLVE, TRAIN = MODE == FUSED_O2;
   constexpr int BW = MAX_KEY_BLOCKS / 32;  // mask words per wave
   __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) E vbuf[FUSED ? 2 : 1][FUSED ? TV::ELEMS : 8];
   // bit kb of word kb / 32: key block kb holds a positive probability for
   // one of the wave's 32 rows
   __shared__ uint32_t bits[TAU_WAVES * BW];
@@ -167,6 +178,7 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
     int cmax = 0;        // wave maximum of cc once the cache is in use
     bool small_support = false;  // every thread's support count <= cap / 2
     float f_prev = INFINITY;     // |f| at the previous evaluation
+    float usum = 0.f;            // sum of u = z^(gamma-1) over the row at the last tau
     for (int it = 0;; ++it) {
       // ---- evaluation at tau: m0 = sum z^gamma, m1 = sum z^(gamma-1),
       // m2 = sum z^(gamma-2) over the strict support z > 0, and mc = the size
@@ -314,6 +326,7 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
       m0 += __shfl_xor(m0, 32);
       m1 += __shfl_xor(m1, 32);
       m2 += __shfl_xor(m2, 32);
+      usum = m1;
 
       const float f = m0 - 1.f;                        // Eq. 3
       float f1, f2;                                    // Eq. 6, 7
@@ -363,6 +376,88 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
       }
     }
 
+    if (row_ok && lane < 32) a.tau[(size_t)bh * n + i] = tau;
+
+    if constexpr (FUSED) {
+      // ---- Algorithm 2 at the returned tau: O = sum_j P_ij V_j, and in
+      // training O2 = sum_j u_ij V_j / sum_j u_ij (sum u is the solver's last
+      // S1 sum), over every valid key block.
+      f32x16 o[NTD], o2[NTD];
+#pragma unroll
+      for (int t = 0; t < NTD; ++t) {
+        o[t] = zero16();
+        if constexpr (TRAIN) o2[t] = zero16();
+      }
+      const E* V = static_cast<const E*>(a.v) + (size_t)bh * n * D;
+      TileDma<TV, D, TAU_NT> vdma;
+      vdma.init();
+      auto pv_tile = [&](const f32x16& s, const E* vt, int sub) {
+        float p[16], u[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float zp = relu_z(c, s[r], tau);
+          if constexpr (TRAIN)
+            Gamma<GK>::pu(zp, g, p[r], u[r]);
+          else
+            p[r] = Gamma<GK>::p_only(zp, g);
+        }
+#pragma unroll
+        for (int t = 0; t < PS; ++t) {
+          const typename M::frag pa = M::pack(p, t);
+          typename M::frag uh, ul;
+          if constexpr (TRAIN) M::pack_split(u, t, uh, ul);
+#pragma unroll
+          for (int nt = 0; nt < NTD; ++nt) {
+            const typename M::frag vb = lds_perm_frag<E, D>(vt, 32 * nt, 32 * sub, t);
+            o[nt] = M::mma(pa, vb, o[nt]);
+            if constexpr (TRAIN) {
+              o2[nt] = M::mma(uh, vb, o2[nt]);
+              if constexpr (!M::exact_operands) o2[nt] = M::mma(ul, vb, o2[nt]);
+            }
+          }
+        }
+      };
+      dma.issue(kbuf[0], K, 0, n);
+      vdma.issue(vbuf[0], V, 0, n);
+      for (int kb = 0; kb < nkb; ++kb) {
+        dma_wait();
+        __syncthreads();
+        if (kb + 1 < nkb) {
+          dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
+          vdma.issue(vbuf[(kb + 1) & 1], V, (kb + 1) * BLK, n);
+        }
+        const int j0 = kb * BLK;
+        const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
+        if (k0 == 0 && k1 == 0) continue;
+        f32x16 s0, s1;
+        scores(kbuf[kb & 1], s0, s1);
+        if (k0 == 2) mask_tile(s0, j0);
+        if (k1 == 2) mask_tile(s1, j0 + 32);
+        if (k0) pv_tile(s0, vbuf[kb & 1], 0);
+        if (k1) pv_tile(s1, vbuf[kb & 1], 1);
+      }
+      if (!wave_ok) return;
+      // accumulator value r of lane l: query q0 + crow(r), column 32 nt + l % 32
+      E* O = static_cast<E*>(a.o) + (size_t)bh * n * D;
+      float* O2 = TRAIN ? a.o2 + (size_t)bh * n * D : nullptr;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = crow(r);
+        const int ir = q0 + row;
+        float us = 0.f;
+        if constexpr (TRAIN) us = __shfl(usum, row);
+        if (ir < n) {
+#pragma unroll
+          for (int nt = 0; nt < NTD; ++nt) {
+            const size_t off = (size_t)ir * D + 32 * nt + (lane & 31);
+            O[off] = (E)o[nt][r];
+            if constexpr (TRAIN) O2[off] = us > 0.f ? o2[nt][r] / us : 0.f;
+          }
+        }
+      }
+      return;
+    }
+
     if (cached) {
       // mask bits at the returned tau from the cached entries
       for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
@@ -375,7 +470,6 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
       }
     }
 
-    if (row_ok && lane < 32) a.tau[(size_t)bh * n + i] = tau;
     __syncthreads();
     constexpr int QBLOCKS = TAU_WAVES / 2;  // 64-row mask rows per workgroup
     for (int x = threadIdx.x; x < QBLOCKS * T; x += TAU_NT) {
@@ -391,21 +485,32 @@ __global__ __launch_bounds__(TAU_NT, 4) void tau_solve_kernel(TauArgs a) {
   }
 }
 
-template <typename E, int D>
+template <typename E, int D, int MODE>
 hipError_t launch_tau_d(const TauArgs& a, hipStream_t s) {
   dim3 grid((unsigned)(a.BH * ((a.n + TAU_ROWS - 1) / TAU_ROWS))), block(TAU_NT);
-  auto kernel = tau_solve_kernel<E, D, 0>;
-  if (a.gk == 1) kernel = tau_solve_kernel<E, D, 1>;
-  if (a.gk == 2) kernel = tau_solve_kernel<E, D, 2>;
-  if (a.gk == 4) kernel = tau_solve_kernel<E, D, 4>;
+  auto kernel = tau_solve_kernel<E, D, 0, MODE>;
+  if (a.gk == 1) kernel = tau_solve_kernel<E, D, 1, MODE>;
+  if (a.gk == 2) kernel = tau_solve_kernel<E, D, 2, MODE>;
+  if (a.gk == 4) kernel = tau_solve_kernel<E, D, 4, MODE>;
   return launch_kernel(kernel, grid, block, s, a);
+}
+
+template <int MODE>
+hipError_t launch_tau_mode(const TauArgs& a, int dtype, int head_dim, hipStream_t s) {
+  if (dtype == 0)
+    return head_dim == 64 ? launch_tau_d<__bf16, 64, MODE>(a, s) : launch_tau_d<__bf16, 128, MODE>(a, s);
+  return head_dim == 64 ? launch_tau_d<float, 64, MODE>(a, s) : launch_tau_d<float, 128, MODE>(a, s);
 }
 
 }  // namespace
 
 hipError_t launch_tau(const TauArgs& a, int dtype, int head_dim, hipStream_t s) {
-  if (dtype == 0) return head_dim == 64 ? launch_tau_d<__bf16, 64>(a, s) : launch_tau_d<__bf16, 128>(a, s);
-  return head_dim == 64 ? launch_tau_d<float, 64>(a, s) : launch_tau_d<float, 128>(a, s);
+  return launch_tau_mode<SOLVE>(a, dtype, head_dim, s);
+}
+
+hipError_t launch_tau_fused(const TauArgs& a, int dtype, int head_dim, hipStream_t s) {
+  return a.o2 ? launch_tau_mode<FUSED_O2>(a, dtype, head_dim, s)
+              : launch_tau_mode<FUSED_O>(a, dtype, head_dim, s);
 }
 
 }  // namespace ea

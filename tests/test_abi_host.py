@@ -168,3 +168,24 @@ def test_rows_validation():
     b = ea.entmax_rows_bwd
     assert b(4, 100, ea.EA_BF16, p, _fake(), _fake(), None, _fake(), None) == ea.EA_ERR_INVALID_ARG
     assert b(4, 100, ea.EA_BF16, p, _fake(), _fake(), _fake(), None, None) == ea.EA_ERR_INVALID_ARG
+
+
+def test_dense_mode_validation():
+    s, p = shape(), ea.default_params()
+    f = ea._lib.entmax_attn_fwd_dense
+    # null tau
+    assert f(s, p, _fake(), _fake(), _fake(), _fake(), None, _fake(), None, 0, None) == \
+        ea.EA_ERR_INVALID_ARG
+    # o2 required while need_bwd
+    assert f(s, p, _fake(), _fake(), _fake(), _fake(), _fake(), None, None, 0, None) == \
+        ea.EA_ERR_INVALID_ARG
+    # misaligned workspace
+    assert f(s, p, _fake(), _fake(), _fake(), _fake(), _fake(), _fake(), _fake() + 8, 64, None) == \
+        ea.EA_ERR_INVALID_ARG
+    b = ea._lib.entmax_attn_bwd_dense
+    z = ea.entmax_attn_sizes(s, p)
+    args = [_fake()] * 4
+    assert b(s, p, *args, _fake(), _fake(), _fake(), _fake(), _fake(), _fake(), z.ws_bwd - 4,
+             None) == ea.EA_ERR_WORKSPACE
+    assert b(s, p, *args, None, _fake(), _fake(), _fake(), _fake(), _fake(), z.ws_bwd,
+             None) == ea.EA_ERR_INVALID_ARG
