@@ -106,13 +106,14 @@ ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_s
  *   o        [BH, n, d] in shape->dtype, 16-byte aligned (written)
  *   res      residual buffers (written), 4-byte aligned, o2 16-byte aligned
  *   workspace optional, 16-byte aligned: the solver's candidate cache, one
- *            256 KiB slot per 128-row query tile (sizes.ws_fwd covers all
- *            tiles).  A tile with a slot, once its rows' brackets have
- *            narrowed, stores the scores above each row's lower bracket end
- *            and runs its remaining evaluations on them instead of
- *            streaming K again; tiles without one (all of them for NULL)
- *            stream K on every pass.  Results agree up to rounding either
- *            way.  Contents are scratch.
+ *            768 KiB slot per 256-row query tile (sizes.ws_fwd covers all
+ *            tiles).  A tile with a slot stores, while it finds the row
+ *            maxima, the scores above each row's lower bracket end and runs
+ *            its evaluations on them instead of streaming K again (when the
+ *            stored scores do not fit, it streams K, and tries once more
+ *            after its brackets have narrowed); tiles without one (all of
+ *            them for NULL) stream K on every pass.  Results agree up to
+ *            rounding either way.  Contents are scratch.
  * Launches 3 kernels on `stream`.
  */
 ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const void* q,

@@ -21,9 +21,12 @@ namespace {
 constexpr int DEFAULT_MAX_ITER = 12;
 constexpr float DEFAULT_TOL = 1e-5f;
 constexpr int MAX_ITER_CAP = 64;
-// Candidate-cache entries per solver thread (see entmax_attn_sizes).
-constexpr int TAU_CACHE_CAP = 128;
-constexpr size_t TAU_SLOT_BYTES = (size_t)TAU_CACHE_CAP * TAU_THREADS * sizeof(CandEntry);
+// Candidate-cache entries per list (see entmax_attn_sizes); a slot holds
+// two lists per row of a workgroup.
+constexpr int TAU_CACHE_CAP = 192;
+static_assert(TAU_CACHE_CAP % 8 == 0, "the solver reads lists in batches of 8 entries");
+constexpr size_t SOLVE_SLOT_BYTES = (size_t)TAU_CACHE_CAP * 2 * SOLVE_ROWS * sizeof(CandEntry);
+constexpr size_t TAU_SLOT_BYTES = (size_t)TAU_CACHE_CAP * 2 * TAU_ROWS * sizeof(CandEntry);
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -69,8 +72,12 @@ ea_status check_shape(const ea_shape* s, const ea_params* p, Dims* out) {
 // delta, one fp32 per row
 size_t bwd_ws_bytes(const Dims& d) { return (size_t)(d.BH * d.n) * 4; }
 
-// One cache slot per 128-row solver tile.
+// One cache slot per solver workgroup: 256-row tiles for the masked path,
+// 128-row tiles for the no-mask fused forward.  The masked path's sizing
+// covers both.
+int64_t solve_slots(const Dims& d) { return d.BH * ((d.n + SOLVE_ROWS - 1) / SOLVE_ROWS); }
 int64_t cache_slots(const Dims& d) { return d.BH * ((d.n + TAU_ROWS - 1) / TAU_ROWS); }
+static_assert(SOLVE_ROWS == 2 * TAU_ROWS, "a masked-path slot covers two fused-forward slots");
 
 void fill_sizes(const Dims& d, ea_sizes* z) {
   z->tau = (size_t)(d.BH * d.n) * 4;
@@ -81,7 +88,7 @@ void fill_sizes(const Dims& d, ea_sizes* z) {
   z->k_count = z->q_count;
   z->k_index = z->q_index;
   z->stats = (size_t)(d.BH * d.T) * 4;
-  z->ws_fwd = (size_t)cache_slots(d) * TAU_SLOT_BYTES;
+  z->ws_fwd = (size_t)solve_slots(d) * SOLVE_SLOT_BYTES;
   z->ws_bwd = bwd_ws_bytes(d);
 }
 
@@ -180,8 +187,8 @@ ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const
   if (stage == 0) {
     // The cache is optional: tiles without a slot (all of them when there is
     // no workspace) stream K on every solver pass.
-    int64_t slots = workspace ? (int64_t)(ws_bytes / TAU_SLOT_BYTES) : 0;
-    const int64_t most = cache_slots(d);
+    int64_t slots = workspace ? (int64_t)(ws_bytes / SOLVE_SLOT_BYTES) : 0;
+    const int64_t most = solve_slots(d);
     if (slots > most) slots = most;
     CandEntry* cand = slots > 0 ? static_cast<CandEntry*>(workspace) : nullptr;
     TauArgs ta{q, k, res->tau, res->block_mask, res->stats, nullptr, nullptr, nullptr, cand,

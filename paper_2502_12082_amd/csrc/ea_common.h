@@ -43,6 +43,24 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 // Row of accumulator value r for the calling lane (see the layout note above).
 __device__ __forceinline__ int crow(int r) { return 8 * (r >> 2) + 4 * (lane_id() >> 5) + (r & 3); }
 
+// The values that lanes l % 32 and 32 + l % 32 hold in v (the two halves of
+// the wave exchange with one v_permlane32_swap, no LDS round trip).
+__device__ __forceinline__ void wave_halves(float v, float& lo, float& hi) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+#else
+  lo = hi = v;
+#endif
+}
+// v of lane l plus v of lane l ^ 32, the same value in both lanes.
+__device__ __forceinline__ float sum_halves(float v) {
+  float lo, hi;
+  wave_halves(v, lo, hi);
+  return lo + hi;
+}
+
 __device__ __forceinline__ f32x16 zero16() {
   f32x16 z;
 #pragma unroll

@@ -16,14 +16,19 @@ constexpr int MAX_KEY_BLOCKS = MAX_SEQLEN / 64;
 // {1, 2, 4} run without transcendentals; 0 means general alpha.
 int gamma_kind(float alpha);
 
-// One cached score of the solver: x = (alpha-1) * scale * <q_i, k_j> and the
-// key block of j.
+// One cached score of the solver: the raw score s = <q_i, k_j> (the solver
+// forms x - tau from it exactly as in a streamed evaluation) and the key
+// block of j.
 struct alignas(8) CandEntry {
-  float x;
+  float s;
   int32_t kb;
 };
 
-// Solver workgroup geometry (rows per workgroup, threads per workgroup).
+// Workgroup geometry (rows and threads per workgroup) of the masked path's
+// solver and of the no-mask fused forward.  Each row has two candidate
+// lists (one per half of every key block), of `cap` entries each.
+constexpr int SOLVE_ROWS = 256;
+constexpr int SOLVE_THREADS = 256;
 constexpr int TAU_ROWS = 128;
 constexpr int TAU_THREADS = 256;
 
@@ -38,9 +43,9 @@ struct TauArgs {
   const void* v;
   void* o;            // [BH, n, D] input dtype
   float* o2;          // [BH, n, D] fp32, or null (inference)
-  CandEntry* cand;    // candidate cache: [slots][cap][TAU_THREADS], or null
-  int cap;            // entries per thread
-  int slots;          // 128-row tiles with a cache slot (tile t uses slot t)
+  CandEntry* cand;    // candidate cache: one slot of 2 * rows * cap entries per workgroup, or null
+  int cap;            // entries per list
+  int slots;          // workgroups with a cache slot (workgroup t uses slot t)
   int BH, n, T;
   float c;            // (alpha - 1) * scale
   float alpha, gamma;

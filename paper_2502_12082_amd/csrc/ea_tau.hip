@@ -8,10 +8,13 @@
 // bisection rule B_f (Eq. 4) and the Halley step H_f (Eq. 5) is taken when it
 // lands inside the bracket, otherwise the midpoint.  The bracket starts at
 // [max_j x_ij - 1, max_j x_ij - n_i^(1-alpha)] after a first pass that finds
-// the row maximum.  The block mask of Eq. 8 is recorded during every
-// evaluation pass; the pass at the returned tau is the last one, so the mask
-// describes exactly the probabilities that the forward and backward kernels
-// recompute from that tau.
+// the row maximum; that pass also raises the lower end with the largest
+// scores' own bound (see pass 0) and, given a workspace, collects each row's
+// scores above it, on which every later evaluation can run without K.  The
+// block mask of Eq. 8 is recorded during every evaluation (or rebuilt from
+// the collected scores) at the returned tau, so the mask describes exactly
+// the probabilities that the forward and backward kernels recompute from
+// that tau.
 //
 // Layout on gfx950: one workgroup = 4 waves = 128 query rows (two mask
 // rows); each wave keeps its 32 query rows as MFMA B operands in registers
@@ -139,11 +142,25 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
     };
 
     // ---- pass 0: row maximum of the raw scores (scale > 0, so the maximum
-    // of x = c s is c times the maximum of s)
-    float smax = -INFINITY;
-    auto max_tile = [&](const f32x16& s) {
+    // of x = c s is c times the maximum of s), and a tighter lower end of
+    // the bracket: if j distinct keys score at least v, each of their terms
+    // of f is at least (c v - tau)^gamma at any tau below c v, so at the root
+    // j (c v - tau)^gamma <= 1 and tau >= c v - j^(-1/gamma).  j = 1 with v
+    // the maximum is Algorithm 1's tau >= max - 1.  Each lane keeps the four
+    // largest maxima of its 16-score sub-tile columns (each over keys of its
+    // own); the two lanes of a row merge theirs into the row's eight largest,
+    // and v_j is the j-th of those.
+    float t4[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};  // descending
+    auto tile_max = [&](const f32x16& s) {
+      float v = fmaxf(s[0], s[1]);
 #pragma unroll
-      for (int r = 0; r < 16; r += 2) smax = fmaxf(smax, fmaxf(s[r], s[r + 1]));
+      for (int r = 2; r < 16; r += 2) v = fmaxf(v, fmaxf(s[r], s[r + 1]));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float h = fmaxf(t4[j], v);
+        v = fminf(t4[j], v);
+        t4[j] = h;
+      }
     };
     stream([&](int kb, const E* kt) {
       const int j0 = kb * BLK;
@@ -151,24 +168,40 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
       if (k0 == 0 && k1 == 0) return;
       f32x16 s0, s1;
       scores(kt, s0, s1);
-      if (k0 == 1 && k1 == 1) {
-        max_tile(s0);
-        max_tile(s1);
-        return;
-      }
       if (k0 == 2) mask_tile(s0, j0);
       if (k1 == 2) mask_tile(s1, j0 + 32);
-      if (k0) max_tile(s0);
-      if (k1) max_tile(s1);
+      if (k0) tile_max(s0);
+      if (k1) tile_max(s1);
     });
-    smax = fmaxf(smax, __shfl_xor(smax, 32));
 
     float lo = 0.f, hi = 0.f, tau = 0.f;
-    if (row_ok) {
-      const float m = c * smax;
-      lo = m - 1.f;
-      hi = m - powf((float)ni, 1.f - a.alpha);
-      tau = 0.5f * (lo + hi);
+    {
+      // the row's eight largest sub-tile maxima, descending: the two lanes'
+      // sorted lists merged by Batcher's odd-even network
+      float u[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        u[j] = t4[j];
+        u[4 + j] = __shfl_xor(t4[j], 32);
+      }
+      auto cx = [&](int x, int y) {
+        const float h = fmaxf(u[x], u[y]);
+        u[y] = fminf(u[x], u[y]);
+        u[x] = h;
+      };
+      cx(0, 4); cx(1, 5); cx(2, 6); cx(3, 7);
+      cx(2, 4); cx(3, 5);
+      cx(1, 2); cx(3, 4); cx(5, 6);
+      if (row_ok) {
+        const float m = c * u[0];
+        hi = m - powf((float)ni, 1.f - a.alpha);
+        float b = m - 1.f;
+#pragma unroll
+        for (int j = 1; j < 8; ++j) b = fmaxf(b, fmaf(c, u[j], -exp2f(-__log2f((float)(j + 1)) / g)));
+        // the bound may round above the root by an ulp (constant rows reach it)
+        lo = fminf(b - 1e-6f * fmaxf(1.f, fabsf(b)), hi);
+        tau = 0.5f * (lo + hi);
+      }
     }
 
     int passes = 1;      // K passes (streamed), the max pass included
@@ -176,6 +209,21 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
     int attempts = 0;    // cache fills tried
     int cc = 0;          // candidates this thread found in the last fill
     int cmax = 0;        // wave maximum of cc once the cache is in use
+    __shared__ int fill_full;  // some list of the current fill overflowed
+    CandEntry* const mine = cache ? cache + threadIdx.x : nullptr;
+    // Reads this thread's list in batches of eight independent loads and
+    // calls `use` on each entry; the trip count is the wave's longest list.
+    auto scan = [&](auto&& use) {
+      for (int e0 = 0; e0 < cmax; e0 += 8) {
+        CandEntry ce[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (e0 + u < cc) ce[u] = mine[(size_t)(e0 + u) * TAU_NT];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (e0 + u < cc) use(ce[u]);
+      }
+    };
     bool small_support = false;  // every thread's support count <= cap / 2
     float f_prev = INFINITY;     // |f| at the previous evaluation
     float usum = 0.f;            // sum of u = z^(gamma-1) over the row at the last tau
@@ -243,23 +291,34 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
       };
       // Appends the entries x > lo of a sub-tile to this thread's cache list.
       // Every later tau stays >= lo, so the entries left out are 0 there.
-      const float s_lo = row_ok ? lo / c : INFINITY;  // rows past n collect nothing
-      CandEntry* const mine = cache + threadIdx.x;
+      // The threshold in score units carries a margin for the rounding of
+      // lo / c (a superset of the entries is harmless).
+      const float s_lo0 = lo / c;
+      const float s_lo = row_ok ? s_lo0 - 1e-6f * fmaxf(fabsf(s_lo0), 1.f / c) : INFINITY;
       auto fill_tile = [&](const f32x16& s, int kb) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           if (s[r] > s_lo) {
-            if (cc < a.cap) mine[cc * TAU_NT] = CandEntry{c * s[r], kb};
+            if (cc < a.cap) mine[(size_t)cc * TAU_NT] = CandEntry{s[r], kb};
             ++cc;
           }
         }
       };
+      // Decides, after a fill, whether every list fit.
+      auto fill_done = [&]() {
+        if (!__syncthreads_or(cc > a.cap)) {
+          cached = true;
+          cmax = cc;
+#pragma unroll
+          for (int o = 32; o >= 1; o >>= 1) cmax = max(cmax, __shfl_xor(cmax, o));
+        }
+      };
 
-      // From the second evaluation on, a tile with a cache slot tries (at
-      // most twice) to collect its candidates x > lo in a K pass of their
-      // own, when the last streamed evaluation suggests that they fit; the
-      // evaluation at tau then runs on the cache.  If a thread's list
-      // overflows, this evaluation streams K as usual.
+      // A tile with a cache slot collects its candidates x > lo during the
+      // first evaluation; if a list overflows, it tries (once more) later in
+      // a K pass of its own, when the last streamed evaluation suggests that
+      // they fit, and that evaluation then runs on the cache.  Otherwise the
+      // evaluation streams K.
       if (!cached && cache && it >= 1 && attempts < 2 && small_support) {
         ++attempts;
         cc = 0;
@@ -275,26 +334,33 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
           if (k1) fill_tile(s1, kb);
         });
         ++passes;
-        if (!__syncthreads_or(cc > a.cap)) {
-          cached = true;
-          cmax = cc;
-#pragma unroll
-          for (int o = 32; o >= 1; o >>= 1) cmax = max(cmax, __shfl_xor(cmax, o));
-        }
+        fill_done();
       }
       if (!cached) {
         // streamed evaluation; the mask bits of every block are rewritten
+        const bool fill = cache && it == 0;
+        if (fill) {
+          ++attempts;
+          cc = 0;
+          if (threadIdx.x == 0) fill_full = 0;  // read after the first block's barrier
+        }
         uint32_t word = 0;  // mask bits of the current 32-block group (wave-uniform)
         stream([&](int kb, const E* kt) {
           const int j0 = kb * BLK;
           const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
           bool any = false;
+          // once a list of this fill has overflowed, no thread stores more
+          const bool fill_now = fill && !fill_full;
           if (k0 == 1 && k1 == 1) {  // every key valid: one straight-line block
             f32x16 s0, s1;
             scores(kt, s0, s1);
             const bool a0 = eval_tile(s0);
             const bool a1 = eval_tile(s1);
             any = a0 || a1;
+            if (fill_now) {
+              fill_tile(s0, kb);
+              fill_tile(s1, kb);
+            }
           } else if (k0 != 0 || k1 != 0) {
             f32x16 s0, s1;
             scores(kt, s0, s1);
@@ -302,7 +368,12 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
             if (k1 == 2) mask_tile(s1, j0 + 32);
             if (k0) any |= eval_tile(s0);
             if (k1) any |= eval_tile(s1);
+            if (fill_now) {
+              if (k0) fill_tile(s0, kb);
+              if (k1) fill_tile(s1, kb);
+            }
           }
+          if (fill_now && cc > a.cap) fill_full = 1;
           if (__ballot(any) != 0ull) word |= 1u << (kb & 31);
           if ((kb & 31) == 31 || kb == nkb - 1) {
             if (lane == 0) bits[w * BW + (kb >> 5)] = word;
@@ -312,14 +383,15 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
         ++passes;
         // support sizes at this tau, a guide to the size of the candidate lists
         small_support = !__syncthreads_or(mc > a.cap / 2);
+        if (fill) {
+          if (fill_full) cc = a.cap + 1;  // the fill stopped early: its lists are incomplete
+          fill_done();
+        }
       } else {
         // cached evaluation: the same sums over this thread's list
-        for (int e = 0; e < cmax; ++e) {
-          if (e < cc) {
-            const CandEntry ce = cache[(size_t)e * TAU_NT + threadIdx.x];
-            add_z(__builtin_amdgcn_fmed3f(ce.x - tau, 0.f, 1.f), m0, m1, m2, mc);
-          }
-        }
+        scan([&](const CandEntry& ce) {
+          add_z(relu_z(c, ce.s, tau), m0, m1, m2, mc);
+        });
       }
       if constexpr (GK == 1) m1 = (float)mc;
       if constexpr (GK == 2) m2 = (float)mc;
@@ -462,12 +534,9 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
       // mask bits at the returned tau from the cached entries
       for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
       __syncthreads();
-      for (int e = 0; e < cmax; ++e) {
-        if (e < cc) {
-          const CandEntry ce = cache[(size_t)e * TAU_NT + threadIdx.x];
-          if (ce.x - tau > 0.f) atomicOr(&bits[w * BW + (ce.kb >> 5)], 1u << (ce.kb & 31));
-        }
-      }
+      scan([&](const CandEntry& ce) {
+        if (in_support(relu_z(c, ce.s, tau))) atomicOr(&bits[w * BW + (ce.kb >> 5)], 1u << (ce.kb & 31));
+      });
     }
 
     __syncthreads();
@@ -485,6 +554,544 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
   }
 }
 
+// ----------------------------------------------------------- masked solver
+//
+// The solver of the masked path (tau, the block mask and stats).  One
+// workgroup = 4 waves = 256 query rows; wave w owns the 64-row query block
+// qb = 4 qt + w, i.e. one row of the block mask, as two groups of 32 rows
+// (g = 0, 1) that are the B operands of its MFMAs.  Every K fragment read
+// from LDS feeds two MFMAs (one per group), so a pass reads the K tile from
+// LDS half as often per product as with one group per wave; lane l holds
+// query l % 32 of each group, so every lane keeps two rows' sums.  The
+// evaluation, bracket and cache rules are those of tau_solve_kernel.
+constexpr int SV_WAVES = SOLVE_THREADS / 64;
+constexpr int SV_NT = SOLVE_THREADS;
+constexpr int SV_ROWS = SOLVE_ROWS;
+static_assert(SV_ROWS == 64 * SV_WAVES, "one 64-row query block per wave");
+
+// fp32 operands at d = 128 (128 registers of query fragments) run one wave
+// per SIMD; every other variant fits two.
+template <typename E, int D, int GK>
+__global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void solve_kernel(TauArgs a) {
+  using TL = PadTile<E, D>;
+  using M = Mma<E>;
+  constexpr int KS = D / M::KW;
+  constexpr int BW = MAX_KEY_BLOCKS / 32;  // mask words per wave
+  __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
+  // bit kb of word kb / 32: key block kb holds a positive probability for a
+  // row of the wave's query block
+  __shared__ uint32_t bits[SV_WAVES * BW];
+  __shared__ int fill_full;  // some list of the current fill overflowed
+
+  const int lane = lane_id(), w = wave_id();
+  const int n = a.n, T = a.T;
+  const int nqt = (n + SV_ROWS - 1) / SV_ROWS;
+  const int TW = (T + 31) / 32;
+  const float c = a.c, g = a.gamma;
+  const bool newton_bound = g >= 1.f;  // f convex: Newton steps bound the root from below
+  const int tile = blockIdx.x;
+  const int bh = tile % a.BH;
+  int qt = tile / a.BH;
+  if (a.causal) qt = nqt - 1 - qt;  // longest rows first
+  const int qb = qt * SV_WAVES + w;
+  const int q0 = qb * BLK;
+  const bool wave_ok = q0 < n;
+  int qi[2], ni[2];
+  bool row_ok[2];
+#pragma unroll
+  for (int gq = 0; gq < 2; ++gq) {
+    qi[gq] = q0 + 32 * gq + (lane & 31);
+    row_ok[gq] = qi[gq] < n;
+    ni[gq] = a.causal ? qi[gq] + 1 : n;
+  }
+  const E* Q = static_cast<const E*>(a.q) + (size_t)bh * n * D;
+  const E* K = static_cast<const E*>(a.k) + (size_t)bh * n * D;
+  const int wg_last = min(n, (qt + 1) * SV_ROWS) - 1;
+  const int nkb = a.causal ? wg_last / BLK + 1 : T;
+  // this workgroup's cache slot: list (thread t, group gq) holds entry e at
+  // [(2 e + gq) * SV_NT + t]; null without a slot
+  CandEntry* const cache =
+      a.cand && tile < a.slots ? a.cand + (size_t)tile * a.cap * 2 * SV_NT : nullptr;
+
+  TileDma<TL, D, SV_NT> dma;
+  dma.init();
+
+  typename M::frag qf[2][KS];
+#pragma unroll
+  for (int gq = 0; gq < 2; ++gq)
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) qf[gq][kk] = load_row_frag_global<E, D>(Q, qi[gq], n, kk);
+
+  for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
+
+  // Streams every key block in order, double-buffered: block kb + 1 is
+  // copied into LDS while body(kb, tile) works on block kb.  The candidate
+  // lists keep this order, so a cached evaluation adds the same terms in the
+  // same order as a streamed one.
+  auto stream = [&](auto&& body) {
+    dma.issue(kbuf[0], K, 0, n);
+    for (int kb = 0; kb < nkb; ++kb) {
+      dma_wait();
+      __syncthreads();
+      if (kb + 1 < nkb) dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
+      body(kb, kbuf[kb & 1]);
+    }
+    __syncthreads();  // the next pass refills buffer 0
+  };
+
+  // S^T sub-tiles of the staged block: s[h][gq] = keys [32 h, 32 h + 32) x
+  // query group gq; value r of lane l is key 32 h + crow(r), query l % 32 of
+  // the group.  Four independent accumulation chains.
+  auto scores = [&](const E* kt, f32x16 (&s)[2][2]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      s[h][0] = zero16();
+      s[h][1] = zero16();
+    }
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const typename M::frag a0 = lds_row_frag_pad<E, D>(kt, (lane & 31), kk);
+      const typename M::frag a1 = lds_row_frag_pad<E, D>(kt, 32 + (lane & 31), kk);
+      s[0][0] = M::mma(a0, qf[0][kk], s[0][0]);
+      s[0][1] = M::mma(a0, qf[1][kk], s[0][1]);
+      s[1][0] = M::mma(a1, qf[0][kk], s[1][0]);
+      s[1][1] = M::mma(a1, qf[1][kk], s[1][1]);
+    }
+  };
+  // Sub-tile state: 0 = nothing valid, 1 = all valid, 2 = per-element masking.
+  auto sub_kind = [&](int j0, int gq) {
+    const int r0 = q0 + 32 * gq, r1 = min(n - 1, r0 + 31);
+    if (r0 >= n || j0 >= n || (a.causal && j0 > r1)) return 0;
+    if (j0 + 31 >= n || (a.causal && j0 + 31 > r0)) return 2;
+    return 1;
+  };
+  // Invalid keys of a masked sub-tile become -inf: never the maximum, and
+  // the clamp of [x - tau]_+ makes them exactly 0.
+  auto mask_tile = [&](f32x16& s, int j0, int gq) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = j0 + crow(r);
+      if (!(j < n && (!a.causal || j <= qi[gq]))) s[r] = -INFINITY;
+    }
+  };
+  // The block's sub-tiles, scored and masked; returns the kinds (k[h][gq]),
+  // or false when the wave has nothing valid in the block.
+  auto block = [&](int kb, const E* kt, f32x16 (&s)[2][2], int (&k)[2][2]) {
+    const int j0 = kb * BLK;
+    bool anyv = false, all1 = true;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int gq = 0; gq < 2; ++gq) {
+        k[h][gq] = sub_kind(j0 + 32 * h, gq);
+        anyv |= k[h][gq] != 0;
+        all1 &= k[h][gq] == 1;
+      }
+    if (!anyv) return false;
+    scores(kt, s);
+    if (!all1) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int gq = 0; gq < 2; ++gq)
+          if (k[h][gq] == 2) mask_tile(s[h][gq], j0 + 32 * h, gq);
+    }
+    return true;
+  };
+
+  // ---- pass 0: row maxima and the top-eight bound of each row (see
+  // tau_solve_kernel): each lane keeps, per group, the four largest maxima of
+  // its 16-score sub-tile columns.
+  //
+  // With a cache slot, the same pass collects the candidate lists: every
+  // score above the running value of the bound.  Sub-tile maxima only grow,
+  // so the running bound never exceeds the final one, and a list holds every
+  // score above the final lower end of the bracket, which no later tau goes
+  // below.  A wave whose lists come near their capacity filters them by the
+  // current bound; if that frees too little, the workgroup stops collecting
+  // and its evaluations stream K.
+  float t4[2][4];
+#pragma unroll
+  for (int gq = 0; gq < 2; ++gq)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) t4[gq][j] = -INFINITY;
+  float kj[8];  // j^(-1/gamma)
+#pragma unroll
+  for (int j = 0; j < 8; ++j) kj[j] = j == 0 ? 1.f : exp2f(-__log2f((float)(j + 1)) / g);
+  // Inserts the sub-tile's maximum into t4[gq] and returns it.
+  auto tile_max = [&](const f32x16& s, int gq) {
+    float v = fmaxf(s[0], s[1]);
+#pragma unroll
+    for (int r = 2; r < 16; r += 2) v = fmaxf(v, fmaxf(s[r], s[r + 1]));
+    const float top = v;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float h = fmaxf(t4[gq][j], v);
+      v = fminf(t4[gq][j], v);
+      t4[gq][j] = h;
+    }
+    return top;
+  };
+  // The row's eight largest sub-tile maxima, descending: the two lanes'
+  // sorted lists merged by Batcher's odd-even network (the same result in
+  // both lanes of the row).
+  auto row_top8 = [&](int gq, float* u) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) wave_halves(t4[gq][j], u[j], u[4 + j]);
+    auto cx = [&](int x, int y) {
+      const float hv = fmaxf(u[x], u[y]);
+      u[y] = fminf(u[x], u[y]);
+      u[x] = hv;
+    };
+    cx(0, 4); cx(1, 5); cx(2, 6); cx(3, 7);
+    cx(2, 4); cx(3, 5);
+    cx(1, 2); cx(3, 4); cx(5, 6);
+  };
+  // the bound in score units, less a margin that covers the rounding of
+  // x = c s and of the bound itself (a superset of entries is harmless)
+  auto score_bound = [&](const float* u) {
+    float b = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b = fmaxf(b, u[j] - kj[j] / c);
+    return b - 1e-5f * fmaxf(fabsf(b), 1.f / c);
+  };
+
+  int cc[2] = {0, 0};    // entries in this thread's two lists
+  int cmax[2] = {0, 0};  // wave maxima of cc once the cache is in use
+  // Entry e of list gq of this thread sits at byte offset
+  // ((2 e + gq) * SV_NT + t) * 8 of the slot: a 32-bit offset from the
+  // workgroup-uniform slot base.
+  constexpr uint32_t ENTRY_STEP = 2 * SV_NT * sizeof(CandEntry);
+  auto entry_off = [&](int e, int gq) {
+    return (uint32_t)e * ENTRY_STEP + (uint32_t)(gq * SV_NT + (int)threadIdx.x) * sizeof(CandEntry);
+  };
+  auto at = [&](uint32_t off) -> CandEntry& {
+    return *reinterpret_cast<CandEntry*>(reinterpret_cast<char*>(cache) + off);
+  };
+  auto entry = [&](int e, int gq) -> CandEntry& { return at(entry_off(e, gq)); };
+  auto wave_max = [&](int v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o));
+    return v;
+  };
+  // Reads list gq of this thread in batches of eight independent loads,
+  // up to the wave's longest list cmax rounded up to a multiple of 8.  That
+  // stays inside the slot (cmax <= cap, and cap is a multiple of 8); entries
+  // past this thread's own count are stale and never used.
+  auto scan = [&](int gq, auto&& use) {
+    for (int e0 = 0; e0 < cmax[gq]; e0 += 8) {
+      CandEntry ce[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) ce[u] = entry(e0 + u, gq);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (e0 + u < cc[gq]) use(ce[u]);
+    }
+  };
+  // Keeps the entries of list gq above `sb` (all lanes of the wave).
+  auto filter = [&](int gq, float sb) {
+    cmax[gq] = wave_max(cc[gq]);
+    int k = 0;
+    scan(gq, [&](const CandEntry& ce) {
+      if (ce.s > sb) entry(k++, gq) = ce;
+    });
+    cc[gq] = k;
+  };
+  float sb[2] = {-INFINITY, -INFINITY};  // collection thresholds
+  __shared__ int fill_dead;              // a list overflowed: stop collecting
+  if (threadIdx.x == 0) fill_dead = 0;   // read after the first block's barrier
+  stream([&](int kb, const E* kt) {
+    f32x16 s[2][2];
+    int k[2][2];
+    if (!block(kb, kt, s, k)) return;
+    float tm[2][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int gq = 0; gq < 2; ++gq) tm[h][gq] = k[h][gq] ? tile_max(s[h][gq], gq) : -INFINITY;
+    if (!cache || fill_dead) return;
+    if ((kb & 3) == 0) {
+#pragma unroll
+      for (int gq = 0; gq < 2; ++gq) {
+        float u[8];
+        row_top8(gq, u);
+        sb[gq] = row_ok[gq] ? score_bound(u) : INFINITY;
+      }
+    }
+    // a block adds at most 32 entries to each list
+#pragma unroll
+    for (int gq = 0; gq < 2; ++gq) {
+      if (__ballot(cc[gq] > a.cap - 32) != 0ull) {
+        filter(gq, sb[gq]);
+        if (__ballot(cc[gq] > a.cap - 32) != 0ull) {
+          fill_dead = 1;
+          return;
+        }
+      }
+    }
+    // only sub-tiles whose maximum passes in some lane are searched
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int gq = 0; gq < 2; ++gq)
+        if (__ballot(tm[h][gq] > sb[gq]) != 0ull) {
+          uint32_t off = entry_off(cc[gq], gq);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            if (s[h][gq][r] > sb[gq]) {
+              at(off) = CandEntry{s[h][gq][r], kb};
+              off += ENTRY_STEP;
+            }
+          }
+          cc[gq] = (int)((off - entry_off(0, gq)) / ENTRY_STEP);
+        }
+  });
+
+  float lo[2], hi[2], tau[2];
+  float sb_final[2];
+#pragma unroll
+  for (int gq = 0; gq < 2; ++gq) {
+    float u[8];
+    row_top8(gq, u);
+    sb_final[gq] = row_ok[gq] ? score_bound(u) : INFINITY;
+    lo[gq] = hi[gq] = tau[gq] = 0.f;
+    if (row_ok[gq]) {
+      const float m = c * u[0];
+      hi[gq] = m - powf((float)ni[gq], 1.f - a.alpha);
+      float b = m - 1.f;
+#pragma unroll
+      for (int j = 1; j < 8; ++j) b = fmaxf(b, fmaf(c, u[j], -kj[j]));
+      // the bound may round above the root by an ulp (constant rows reach it)
+      lo[gq] = fminf(b - 1e-6f * fmaxf(1.f, fabsf(b)), hi[gq]);
+      tau[gq] = 0.5f * (lo[gq] + hi[gq]);
+    }
+  }
+
+  int passes = 1;  // K passes (streamed), the max pass included
+  // evaluations run on the lists when every one of them fit; the entries
+  // below the final bound (collected while it was still rising) are dropped
+  bool cached = cache && !__syncthreads_or(fill_dead != 0);
+  if (cached) {
+#pragma unroll
+    for (int gq = 0; gq < 2; ++gq) {
+      filter(gq, sb_final[gq]);
+      cmax[gq] = wave_max(cc[gq]);
+    }
+  }
+  int attempts = cache ? 1 : 0;  // cache fills tried (pass 0 is the first)
+  bool small_support = false;    // every list's support count <= cap / 2
+  float f_prev[2] = {INFINITY, INFINITY};
+
+  for (int it = 0;; ++it) {
+    // ---- evaluation at tau (per group): m0 = sum z^gamma, m1 = sum
+    // z^(gamma-1), m2 = sum z^(gamma-2) over the strict support z > 0, mc =
+    // the size of the support.
+    float m0[2] = {0.f, 0.f}, m1[2] = {0.f, 0.f}, m2[2] = {0.f, 0.f};
+    int mc[2] = {0, 0};
+    auto add_z = [&](float zp, int gq) {
+      if constexpr (GK == 1) {
+        m0[gq] += zp;
+        mc[gq] += in_support(zp);
+      } else if constexpr (GK == 2) {
+        m0[gq] = fmaf(zp, zp, m0[gq]);
+        m1[gq] += zp;
+        mc[gq] += in_support(zp);
+      } else if constexpr (GK == 4) {
+        const float z2 = zp * zp;
+        m0[gq] = fmaf(z2, z2, m0[gq]);
+        m1[gq] = fmaf(z2, zp, m1[gq]);
+        m2[gq] += z2;
+        mc[gq] += in_support(zp);
+      } else {
+        if (zp > 0.f) {
+          const float l = __log2f(zp);
+          m0[gq] += exp2f(g * l);
+          m1[gq] += exp2f((g - 1.f) * l);
+          m2[gq] += exp2f((g - 2.f) * l);
+          ++mc[gq];
+        }
+      }
+    };
+    // Adds one sub-tile; returns whether it holds a positive probability.
+    auto eval_tile = [&](const f32x16& s, int gq) {
+      if constexpr (GK == 1 || GK == 2) {
+        int cnt = 0;
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          const float za = relu_z(c, s[r], tau[gq]), zb = relu_z(c, s[r + 1], tau[gq]);
+          if constexpr (GK == 1) {
+            m0[gq] += za;
+            m0[gq] += zb;
+          } else {
+            m0[gq] = fmaf(za, za, m0[gq]);
+            m0[gq] = fmaf(zb, zb, m0[gq]);
+            m1[gq] += za;
+            m1[gq] += zb;
+          }
+          cnt += in_support(za) + in_support(zb);
+        }
+        mc[gq] += cnt;
+        return cnt > 0;
+      } else {
+        bool any = false;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float zp = relu_z(c, s[r], tau[gq]);
+          any |= zp > 0.f;
+          add_z(zp, gq);
+        }
+        return any;
+      }
+    };
+    // Appends the entries x > lo of a sub-tile to list gq; every later tau
+    // stays >= lo, so entries left out are 0 there.  The threshold in score
+    // units carries a margin for the rounding of lo / c.
+    float s_lo[2];
+#pragma unroll
+    for (int gq = 0; gq < 2; ++gq) {
+      const float t0 = lo[gq] / c;
+      s_lo[gq] = row_ok[gq] ? t0 - 1e-6f * fmaxf(fabsf(t0), 1.f / c) : INFINITY;
+    }
+    auto fill_tile = [&](const f32x16& s, int gq, int kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (s[r] > s_lo[gq]) {
+          if (cc[gq] < a.cap) entry(cc[gq], gq) = CandEntry{s[r], kb};
+          ++cc[gq];
+        }
+      }
+    };
+    auto fill_done = [&]() {
+      if (!__syncthreads_or(cc[0] > a.cap || cc[1] > a.cap)) {
+        cached = true;
+        cmax[0] = wave_max(cc[0]);
+        cmax[1] = wave_max(cc[1]);
+      }
+    };
+
+    // If the lists of pass 0 overflowed, collecting them is tried once more
+    // in a K pass of its own, once the last streamed evaluation suggests
+    // that they fit (the brackets have narrowed by then).
+    if (!cached && cache && it >= 1 && attempts < 2 && small_support) {
+      ++attempts;
+      cc[0] = cc[1] = 0;
+      stream([&](int kb, const E* kt) {
+        f32x16 s[2][2];
+        int k[2][2];
+        if (!block(kb, kt, s, k)) return;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int gq = 0; gq < 2; ++gq)
+            if (k[h][gq]) fill_tile(s[h][gq], gq, kb);
+      });
+      ++passes;
+      fill_done();
+    }
+    if (!cached) {
+      // streamed evaluation; the mask bits of every block are rewritten
+      uint32_t word = 0;  // mask bits of the current 32-block group (wave-uniform)
+      stream([&](int kb, const E* kt) {
+        f32x16 s[2][2];
+        int k[2][2];
+        bool any = false;
+        if (block(kb, kt, s, k)) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int gq = 0; gq < 2; ++gq)
+              if (k[h][gq]) any |= eval_tile(s[h][gq], gq);
+        }
+        if (__ballot(any) != 0ull) word |= 1u << (kb & 31);
+        if ((kb & 31) == 31 || kb == nkb - 1) {
+          if (lane == 0) bits[w * BW + (kb >> 5)] = word;
+          word = 0;
+        }
+      });
+      ++passes;
+      small_support = !__syncthreads_or(mc[0] > a.cap / 2 || mc[1] > a.cap / 2);
+    } else {
+#pragma unroll
+      for (int gq = 0; gq < 2; ++gq)
+        scan(gq, [&](const CandEntry& ce) {
+          add_z(relu_z(c, ce.s, tau[gq]), gq);
+        });
+    }
+
+    bool conv = true;
+    float f[2], f1[2], f2[2];
+#pragma unroll
+    for (int gq = 0; gq < 2; ++gq) {
+      if constexpr (GK == 1) m1[gq] = (float)mc[gq];
+      if constexpr (GK == 2) m2[gq] = (float)mc[gq];
+      m0[gq] = sum_halves(m0[gq]);
+      m1[gq] = sum_halves(m1[gq]);
+      m2[gq] = sum_halves(m2[gq]);
+      f[gq] = m0[gq] - 1.f;  // Eq. 3
+      if constexpr (GK == 1) {  // Eq. 6, 7
+        f1[gq] = -m1[gq];
+        f2[gq] = 0.f;
+      } else if constexpr (GK == 2) {
+        f1[gq] = -2.f * m1[gq];
+        f2[gq] = 2.f * m2[gq];
+      } else if constexpr (GK == 4) {
+        f1[gq] = -4.f * m1[gq];
+        f2[gq] = 12.f * m2[gq];
+      } else {
+        f1[gq] = -g * m1[gq];
+        f2[gq] = g * (g - 1.f) * m2[gq];
+      }
+      conv &= !row_ok[gq] || fabsf(f[gq]) <= a.tol;
+    }
+    if (__syncthreads_and(conv) || it >= a.max_iter) break;
+#pragma unroll
+    for (int gq = 0; gq < 2; ++gq) {
+      if (!row_ok[gq]) continue;
+      // the update rules of tau_solve_kernel: B_f (Eq. 4), the Newton lower
+      // bound for convex f, H_f (Eq. 5) with the bracket test and slack, and
+      // for gamma < 1 the midpoint when |f| has not halved
+      if (f[gq] < 0.f)
+        hi[gq] = tau[gq];
+      else
+        lo[gq] = tau[gq];
+      const float slack = 1e-6f * fmaxf(1.f, fmaxf(fabsf(lo[gq]), fabsf(hi[gq])));
+      if (newton_bound && f1[gq] < 0.f) {
+        const float tn = tau[gq] - f[gq] / f1[gq] - 10.f * slack;
+        lo[gq] = fminf(fmaxf(lo[gq], tn), hi[gq]);
+      }
+      const float th = tau[gq] - 2.f * f[gq] * f1[gq] / (2.f * f1[gq] * f1[gq] - f[gq] * f2[gq]);
+      bool take = th >= lo[gq] - slack && th <= hi[gq] + slack;
+      if (!newton_bound && fabsf(f[gq]) > 0.5f * f_prev[gq]) take = false;
+      f_prev[gq] = fabsf(f[gq]);
+      tau[gq] = take ? fminf(fmaxf(th, lo[gq]), hi[gq]) : 0.5f * (lo[gq] + hi[gq]);
+    }
+  }
+
+  if (lane < 32) {
+#pragma unroll
+    for (int gq = 0; gq < 2; ++gq)
+      if (row_ok[gq]) a.tau[(size_t)bh * n + qi[gq]] = tau[gq];
+  }
+
+  if (cached) {
+    // mask bits at the returned tau from the cached entries
+    for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int gq = 0; gq < 2; ++gq)
+      scan(gq, [&](const CandEntry& ce) {
+        if (in_support(relu_z(c, ce.s, tau[gq]))) atomicOr(&bits[w * BW + (ce.kb >> 5)], 1u << (ce.kb & 31));
+      });
+  }
+  __syncthreads();
+  if (!wave_ok) return;
+  for (int kb = lane; kb < T; kb += 64) {
+    const uint8_t b = (bits[w * BW + (kb >> 5)] >> (kb & 31)) & 1u;
+    a.mask[((size_t)bh * T + qb) * T + kb] = b;
+  }
+  if (a.stats && lane == 0) a.stats[(size_t)bh * T + qb] = passes;
+}
+
 template <typename E, int D, int MODE>
 hipError_t launch_tau_d(const TauArgs& a, hipStream_t s) {
   dim3 grid((unsigned)(a.BH * ((a.n + TAU_ROWS - 1) / TAU_ROWS))), block(TAU_NT);
@@ -492,6 +1099,16 @@ hipError_t launch_tau_d(const TauArgs& a, hipStream_t s) {
   if (a.gk == 1) kernel = tau_solve_kernel<E, D, 1, MODE>;
   if (a.gk == 2) kernel = tau_solve_kernel<E, D, 2, MODE>;
   if (a.gk == 4) kernel = tau_solve_kernel<E, D, 4, MODE>;
+  return launch_kernel(kernel, grid, block, s, a);
+}
+
+template <typename E, int D>
+hipError_t launch_solve_d(const TauArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)(a.BH * ((a.n + SV_ROWS - 1) / SV_ROWS))), block(SV_NT);
+  auto kernel = solve_kernel<E, D, 0>;
+  if (a.gk == 1) kernel = solve_kernel<E, D, 1>;
+  if (a.gk == 2) kernel = solve_kernel<E, D, 2>;
+  if (a.gk == 4) kernel = solve_kernel<E, D, 4>;
   return launch_kernel(kernel, grid, block, s, a);
 }
 
@@ -505,7 +1122,9 @@ hipError_t launch_tau_mode(const TauArgs& a, int dtype, int head_dim, hipStream_
 }  // namespace
 
 hipError_t launch_tau(const TauArgs& a, int dtype, int head_dim, hipStream_t s) {
-  return launch_tau_mode<SOLVE>(a, dtype, head_dim, s);
+  if (dtype == 0)
+    return head_dim == 64 ? launch_solve_d<__bf16, 64>(a, s) : launch_solve_d<__bf16, 128>(a, s);
+  return head_dim == 64 ? launch_solve_d<float, 64>(a, s) : launch_solve_d<float, 128>(a, s);
 }
 
 hipError_t launch_tau_fused(const TauArgs& a, int dtype, int head_dim, hipStream_t s) {

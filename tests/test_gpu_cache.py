@@ -83,13 +83,16 @@ def test_cache_against_oracle(alpha):
 
 
 def test_cache_engages_at_high_sparsity():
-    """alpha 1.5, c = 1 on n = 4096: most tiles finish on the cache, so the
-    mean number of K passes drops well below the streaming solver's."""
+    """alpha 1.5, c = 1 on n = 4096: the candidate lists collected during the
+    first evaluation fit, so nearly every tile finishes on the cache after
+    two K passes (the max pass and that evaluation; a tile whose lists
+    overflow streams K instead)."""
     inp = synth.attention_inputs(1, 4, 4096, 128, c=1.0, dtype="bf16", seed=5)
     (o0, r0), (o1, r1) = _both(inp, 1.5, False)
     p0, p1 = r0.stats.float().mean().item(), r1.stats.float().mean().item()
     log("K passes: streaming %.2f, cached %.2f" % (p0, p1))
     assert p1 <= p0 - 1.0
+    assert p1 <= 2.2
     assert torch.equal(r0.block_mask, r1.block_mask) or \
         (r0.block_mask != r1.block_mask).float().mean().item() < 1e-3
 

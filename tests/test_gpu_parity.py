@@ -48,7 +48,9 @@ def test_tiny_forward_fp32():
     """Tiny config: B1 H1 n256 d64 fp32, alpha 1.5, non-causal, forward."""
     gpu, errs = _full_case(1, 1, 256, 64, "f32", 1.5, False, False, 1.0, synth.SEED_BASE,
                            label="tiny")
-    assert gpu["stats"].min() >= 2
+    # the max pass always streams K; with the candidate cache collected in it,
+    # the evaluations need no further K pass
+    assert gpu["stats"].min() >= 1
 
 
 @pytest.mark.parametrize("d", [64, 128])
