@@ -628,16 +628,17 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // copied into LDS while body(kb, tile) works on block kb.  The candidate
   // lists keep this order, so a cached evaluation adds the same terms in the
   // same order as a streamed one.
-  auto stream = [&](auto&& body) {
+  auto stream_n = [&](int count, auto&& body) {
     dma.issue(kbuf[0], K, 0, n);
-    for (int kb = 0; kb < nkb; ++kb) {
+    for (int kb = 0; kb < count; ++kb) {
       dma_wait();
       __syncthreads();
-      if (kb + 1 < nkb) dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
+      if (kb + 1 < count) dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
       body(kb, kbuf[kb & 1]);
     }
     __syncthreads();  // the next pass refills buffer 0
   };
+  auto stream = [&](auto&& body) { stream_n(nkb, body); };
 
   // S^T sub-tiles of the staged block: s[h][gq] = keys [32 h, 32 h + 32) x
   // query group gq; value r of lane l is key 32 h + crow(r), query l % 32 of
@@ -758,17 +759,13 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 
   int cc[2] = {0, 0};    // entries in this thread's two lists
   int cmax[2] = {0, 0};  // wave maxima of cc once the cache is in use
-  // Entry e of list gq of this thread sits at byte offset
-  // ((2 e + gq) * SV_NT + t) * 8 of the slot: a 32-bit offset from the
-  // workgroup-uniform slot base.
-  constexpr uint32_t ENTRY_STEP = 2 * SV_NT * sizeof(CandEntry);
-  auto entry_off = [&](int e, int gq) {
-    return (uint32_t)e * ENTRY_STEP + (uint32_t)(gq * SV_NT + (int)threadIdx.x) * sizeof(CandEntry);
+  // index of entry e of list gq of this thread (32-bit, from the
+  // workgroup-uniform slot base)
+  constexpr uint32_t ENTRY_STEP = 2 * SV_NT;
+  auto entry_idx = [&](int e, int gq) {
+    return (uint32_t)e * ENTRY_STEP + (uint32_t)(gq * SV_NT + (int)threadIdx.x);
   };
-  auto at = [&](uint32_t off) -> CandEntry& {
-    return *reinterpret_cast<CandEntry*>(reinterpret_cast<char*>(cache) + off);
-  };
-  auto entry = [&](int e, int gq) -> CandEntry& { return at(entry_off(e, gq)); };
+  auto put = [&](uint32_t idx, float sv, int kbv) { cache[idx] = CandEntry{sv, kbv}; };
   auto wave_max = [&](int v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o));
@@ -778,28 +775,54 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // up to the wave's longest list cmax rounded up to a multiple of 8.  That
   // stays inside the slot (cmax <= cap, and cap is a multiple of 8); entries
   // past this thread's own count are stale and never used.
-  auto scan = [&](int gq, auto&& use) {
+  // use(score, key block) for each entry of list gq.
+  auto scan_kb = [&](int gq, auto&& use) {
     for (int e0 = 0; e0 < cmax[gq]; e0 += 8) {
       CandEntry ce[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) ce[u] = entry(e0 + u, gq);
+      for (int u = 0; u < 8; ++u) ce[u] = cache[entry_idx(e0 + u, gq)];
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        if (e0 + u < cc[gq]) use(ce[u]);
+        if (e0 + u < cc[gq]) use(ce[u].s, ce[u].kb);
     }
   };
+  auto scan = [&](int gq, auto&& use) { scan_kb(gq, [&](float sv, int) { use(sv); }); };
   // Keeps the entries of list gq above `sb` (all lanes of the wave).
   auto filter = [&](int gq, float sb) {
     cmax[gq] = wave_max(cc[gq]);
     int k = 0;
-    scan(gq, [&](const CandEntry& ce) {
-      if (ce.s > sb) entry(k++, gq) = ce;
+    scan_kb(gq, [&](float sv, int kv) {
+      if (sv > sb) put(entry_idx(k++, gq), sv, kv);
     });
     cc[gq] = k;
   };
   float sb[2] = {-INFINITY, -INFINITY};  // collection thresholds
   __shared__ int fill_dead;              // a list overflowed: stop collecting
   if (threadIdx.x == 0) fill_dead = 0;   // read after the first block's barrier
+  // With a cache slot, a short first stream over the first W key blocks
+  // finds their sub-tile maxima, so that the collection below starts from
+  // a bound close to its final value instead of collecting (and later
+  // dropping) most scores of its first blocks.  Those blocks' maxima are
+  // then not inserted again (the bound needs distinct keys).
+  const int W = cache ? min(nkb, max(1, nkb / 8)) : 0;
+  if (W > 0) {
+    stream_n(W, [&](int kb, const E* kt) {
+      f32x16 s[2][2];
+      int k[2][2];
+      if (!block(kb, kt, s, k)) return;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int gq = 0; gq < 2; ++gq)
+          if (k[h][gq]) tile_max(s[h][gq], gq);
+    });
+#pragma unroll
+    for (int gq = 0; gq < 2; ++gq) {
+      float u[8];
+      row_top8(gq, u);
+      sb[gq] = row_ok[gq] ? score_bound(u) : INFINITY;
+    }
+  }
   stream([&](int kb, const E* kt) {
     f32x16 s[2][2];
     int k[2][2];
@@ -808,7 +831,16 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq) tm[h][gq] = k[h][gq] ? tile_max(s[h][gq], gq) : -INFINITY;
+      for (int gq = 0; gq < 2; ++gq) {
+        if (kb >= W) {
+          tm[h][gq] = k[h][gq] ? tile_max(s[h][gq], gq) : -INFINITY;
+        } else {
+          float v = s[h][gq][0];
+#pragma unroll
+          for (int r = 1; r < 16; ++r) v = fmaxf(v, s[h][gq][r]);
+          tm[h][gq] = k[h][gq] ? v : -INFINITY;
+        }
+      }
     if (!cache || fill_dead) return;
     if ((kb & 3) == 0) {
 #pragma unroll
@@ -835,25 +867,23 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 #pragma unroll
       for (int gq = 0; gq < 2; ++gq)
         if (__ballot(tm[h][gq] > sb[gq]) != 0ull) {
-          uint32_t off = entry_off(cc[gq], gq);
+          uint32_t off = entry_idx(cc[gq], gq);
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             if (s[h][gq][r] > sb[gq]) {
-              at(off) = CandEntry{s[h][gq][r], kb};
+              put(off, s[h][gq][r], kb);
               off += ENTRY_STEP;
             }
           }
-          cc[gq] = (int)((off - entry_off(0, gq)) / ENTRY_STEP);
+          cc[gq] = (int)((off - entry_idx(0, gq)) / ENTRY_STEP);
         }
   });
 
   float lo[2], hi[2], tau[2];
-  float sb_final[2];
 #pragma unroll
   for (int gq = 0; gq < 2; ++gq) {
     float u[8];
     row_top8(gq, u);
-    sb_final[gq] = row_ok[gq] ? score_bound(u) : INFINITY;
     lo[gq] = hi[gq] = tau[gq] = 0.f;
     if (row_ok[gq]) {
       const float m = c * u[0];
@@ -868,15 +898,13 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   }
 
   int passes = 1;  // K passes (streamed), the max pass included
-  // evaluations run on the lists when every one of them fit; the entries
-  // below the final bound (collected while it was still rising) are dropped
+  // Evaluations run on the lists when every one of them fit.  Entries below
+  // the final bound (collected while it was still rising) stay: at any tau
+  // of the bracket their z is clamped to exactly 0, as in a streamed pass.
   bool cached = cache && !__syncthreads_or(fill_dead != 0);
   if (cached) {
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq) {
-      filter(gq, sb_final[gq]);
-      cmax[gq] = wave_max(cc[gq]);
-    }
+    for (int gq = 0; gq < 2; ++gq) cmax[gq] = wave_max(cc[gq]);
   }
   int attempts = cache ? 1 : 0;  // cache fills tried (pass 0 is the first)
   bool small_support = false;    // every list's support count <= cap / 2
@@ -956,7 +984,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         if (s[r] > s_lo[gq]) {
-          if (cc[gq] < a.cap) entry(cc[gq], gq) = CandEntry{s[r], kb};
+          if (cc[gq] < a.cap) put(entry_idx(cc[gq], gq), s[r], kb);
           ++cc[gq];
         }
       }
@@ -1013,9 +1041,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     } else {
 #pragma unroll
       for (int gq = 0; gq < 2; ++gq)
-        scan(gq, [&](const CandEntry& ce) {
-          add_z(relu_z(c, ce.s, tau[gq]), gq);
-        });
+        scan(gq, [&](float sv) { add_z(relu_z(c, sv, tau[gq]), gq); });
     }
 
     bool conv = true;
@@ -1079,8 +1105,8 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     __syncthreads();
 #pragma unroll
     for (int gq = 0; gq < 2; ++gq)
-      scan(gq, [&](const CandEntry& ce) {
-        if (in_support(relu_z(c, ce.s, tau[gq]))) atomicOr(&bits[w * BW + (ce.kb >> 5)], 1u << (ce.kb & 31));
+      scan_kb(gq, [&](float sv, int kv) {
+        if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
       });
   }
   __syncthreads();
