@@ -36,7 +36,7 @@ KERNELS = ("tau_solve", "compact", "fwd_sparse", "bwd_delta", "bwd_dkdv", "bwd_d
 # MFMA block products (64 x 64 x d each) per listed block, by kernel
 PRODUCTS_PER_ACTIVE = {"fwd_sparse": 3, "bwd_dkdv": 4, "bwd_dq": 3}
 # kernel name fragment in profiler output, and the sources that define each kernel
-PROFILE_NAMES = {"tau_solve": "tau_solve_kernel", "fwd_sparse": "fwd_kernel",
+PROFILE_NAMES = {"tau_solve": "solve_kernel", "fwd_sparse": "fwd_kernel",
                  "bwd_dkdv": "dkdv_kernel", "bwd_dq": "dq_kernel"}
 KERNEL_SOURCES = {"tau_solve": ["ea_tau.hip"], "fwd_sparse": ["ea_fwd.hip"],
                   "bwd_dkdv": ["ea_bwd.hip"], "bwd_dq": ["ea_bwd.hip"]}
@@ -239,6 +239,15 @@ class Runner:
         # valid 64x64 blocks each query block streams per solver pass
         per_qb = np.arange(1, T + 1) if self.params.causal else np.full(T, T)
         solver_blocks = float((stats * per_qb[None, :]).sum())
+        # With a candidate-cache slot (the whole workspace is passed here), the
+        # max pass of each 256-row tile first streams its key blocks
+        # 0 .. W-1 once more, W = max(1, nkb / 8) with nkb the tile's key
+        # blocks; stats counts whole passes, so those blocks are added here.
+        for qt in range((n + 255) // 256):
+            nkb = (min(n, 256 * (qt + 1)) - 1) // 64 + 1 if self.params.causal else T
+            w_blocks = max(1, nkb // 8)
+            for qb in range(4 * qt, min(T, 4 * qt + 4)):
+                solver_blocks += BH * min(int(per_qb[qb]), w_blocks)
         flops = {"tau_solve": solver_blocks * f_blk, "compact": 0.0, "bwd_delta": 0.0}
         for k_, m in PRODUCTS_PER_ACTIVE.items():
             flops[k_] = m * n_act * f_blk
