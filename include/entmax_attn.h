@@ -54,7 +54,8 @@ typedef struct {
   float scale;      /* > 0, finite; usually 1/sqrt(head_dim) */
   int32_t causal;   /* 0 or 1 */
   int32_t max_iter; /* Halley-bisection updates after the initial midpoint (Algorithm 1's T), 0..64 */
-  float tol;        /* >= 0: a 128-row workgroup stops once every row has |f(tau)| <= tol */
+  float tol;        /* >= 0: the solver stops on a tile of query rows (256; 128 without a mask)
+                       once every row has |f(tau)| <= tol */
   int32_t need_bwd; /* 1: also write o2 for a later entmax_attn_bwd */
 } ea_params;
 

@@ -747,12 +747,41 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     cx(2, 4); cx(3, 5);
     cx(1, 2); cx(3, 4); cx(5, 6);
   };
+  // Lower end of the bracket (x units) from the row's eight largest
+  // sub-tile maxima u (descending, distinct keys).  One term of f at a time
+  // gives tau >= c u_j - j^(-1/gamma); then two Newton steps on f restricted
+  // to these eight scores.  For gamma >= 1 that restricted f is convex and
+  // decreasing, so Newton steps from a point below its root stay below it,
+  // and its root is itself below tau (the dropped terms of f are >= 0).
+  // Every z here is at most 1, as the per-element maps assume, and z_1 > 0
+  // keeps the derivative nonzero.
+  auto x_bound = [&](const float* u) {
+    float b = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b = fmaxf(b, fmaf(c, u[j], -kj[j]));
+    if (newton_bound && b > -INFINITY) {
+#pragma unroll
+      for (int it = 0; it < 2; ++it) {
+        float f = -1.f, fp = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float z = fmaf(c, u[j], -b);
+          if (z > 0.f) {
+            float pj, uj;
+            Gamma<GK>::pu(z, g, pj, uj);
+            f += pj;
+            fp += uj;
+          }
+        }
+        b += f / (g * fp);
+      }
+    }
+    return b;
+  };
   // the bound in score units, less a margin that covers the rounding of
   // x = c s and of the bound itself (a superset of entries is harmless)
   auto score_bound = [&](const float* u) {
-    float b = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) b = fmaxf(b, u[j] - kj[j] / c);
+    const float b = x_bound(u) / c;
     return b - 1e-5f * fmaxf(fabsf(b), 1.f / c);
   };
 
@@ -888,11 +917,10 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     if (row_ok[gq]) {
       const float m = c * u[0];
       hi[gq] = m - powf((float)ni[gq], 1.f - a.alpha);
-      float b = m - 1.f;
-#pragma unroll
-      for (int j = 1; j < 8; ++j) b = fmaxf(b, fmaf(c, u[j], -kj[j]));
-      // the bound may round above the root by an ulp (constant rows reach it)
-      lo[gq] = fminf(b - 1e-6f * fmaxf(1.f, fabsf(b)), hi[gq]);
+      const float b = x_bound(u);
+      // the bound may round above the root by a few ulps (rows whose whole
+      // support is among the eight reach it)
+      lo[gq] = fminf(b - 4e-6f * fmaxf(1.f, fabsf(b)), hi[gq]);
       tau[gq] = 0.5f * (lo[gq] + hi[gq]);
     }
   }
@@ -1069,7 +1097,12 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       }
       conv &= !row_ok[gq] || fabsf(f[gq]) <= a.tol;
     }
-    if (__syncthreads_and(conv) || it >= a.max_iter) break;
+    // A streamed evaluation has just written the mask bits at this tau, so
+    // the loop ends here.  With cached scores the bits are rebuilt at the
+    // end from the returned tau, so the update from this last evaluation
+    // is still taken: one more Halley step costs nothing there.
+    const bool stop = __syncthreads_and(conv) || it >= a.max_iter;
+    if (stop && !cached) break;
 #pragma unroll
     for (int gq = 0; gq < 2; ++gq) {
       if (!row_ok[gq]) continue;
@@ -1091,6 +1124,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       f_prev[gq] = fabsf(f[gq]);
       tau[gq] = take ? fminf(fmaxf(th, lo[gq]), hi[gq]) : 0.5f * (lo[gq] + hi[gq]);
     }
+    if (stop) break;
   }
 
   if (lane < 32) {
