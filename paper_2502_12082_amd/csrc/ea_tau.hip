@@ -755,11 +755,11 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // and its root is itself below tau (the dropped terms of f are >= 0).
   // Every z here is at most 1, as the per-element maps assume, and z_1 > 0
   // keeps the derivative nonzero.
-  auto x_bound = [&](const float* u) {
+  auto x_bound = [&](const float* u, bool refine) {
     float b = -INFINITY;
 #pragma unroll
     for (int j = 0; j < 8; ++j) b = fmaxf(b, fmaf(c, u[j], -kj[j]));
-    if (newton_bound && b > -INFINITY) {
+    if (refine && newton_bound && b > -INFINITY) {
 #pragma unroll
       for (int it = 0; it < 2; ++it) {
         float f = -1.f, fp = 0.f;
@@ -780,8 +780,8 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   };
   // the bound in score units, less a margin that covers the rounding of
   // x = c s and of the bound itself (a superset of entries is harmless)
-  auto score_bound = [&](const float* u) {
-    const float b = x_bound(u) / c;
+  auto score_bound = [&](const float* u, bool refine) {
+    const float b = x_bound(u, refine) / c;
     return b - 1e-5f * fmaxf(fabsf(b), 1.f / c);
   };
 
@@ -849,7 +849,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     for (int gq = 0; gq < 2; ++gq) {
       float u[8];
       row_top8(gq, u);
-      sb[gq] = row_ok[gq] ? score_bound(u) : INFINITY;
+      sb[gq] = row_ok[gq] ? score_bound(u, true) : INFINITY;
     }
   }
   stream([&](int kb, const E* kt) {
@@ -871,12 +871,15 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         }
       }
     if (!cache || fill_dead) return;
+    // Every 4 blocks the running bound takes the one-term bound of the
+    // current maxima, every 32 blocks the Newton-refined one (any valid
+    // lower bound serves; the first stream already left a close one).
     if ((kb & 3) == 0) {
 #pragma unroll
       for (int gq = 0; gq < 2; ++gq) {
         float u[8];
         row_top8(gq, u);
-        sb[gq] = row_ok[gq] ? score_bound(u) : INFINITY;
+        if (row_ok[gq]) sb[gq] = fmaxf(sb[gq], score_bound(u, (kb & 31) == 0));
       }
     }
     // a block adds at most 32 entries to each list
@@ -917,7 +920,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     if (row_ok[gq]) {
       const float m = c * u[0];
       hi[gq] = m - powf((float)ni[gq], 1.f - a.alpha);
-      const float b = x_bound(u);
+      const float b = x_bound(u, true);
       // the bound may round above the root by a few ulps (rows whose whole
       // support is among the eight reach it)
       lo[gq] = fminf(b - 4e-6f * fmaxf(1.f, fabsf(b)), hi[gq]);
