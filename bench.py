@@ -75,10 +75,11 @@ def measured_traffic(kernel):
     return float(fields["hbm_bytes_per_launch"])
 
 
-def write_traffic(fetch_csv, write_csv, calib_mib, command):
+def write_traffic(fetch_csv, write_csv, calib_mib, command, head_dim=128):
     """Scale each kernel's FETCH_SIZE and WRITE_SIZE (KiB per dispatch) by what
     the same counter reads for the plain copy of `calib_mib` MiB, and write
-    one summary per kernel into profiles/."""
+    one summary per kernel into profiles/.  Only the bf16 instantiations for
+    `head_dim` (the headline workload's) are counted."""
     import csv
     import collections
 
@@ -100,7 +101,7 @@ def write_traffic(fetch_csv, write_csv, calib_mib, command):
     f_scale = calib_kib / max(fetch[cname])
     w_scale = calib_kib / max(write[cname])
     for kernel, frag in PROFILE_NAMES.items():
-        names = [k for k in fetch if frag in k]
+        names = [k for k in fetch if frag in k and ("DF16bLi%dE" % head_dim) in k]
         if not names:
             continue
         fk = [v for k in names for v in fetch[k]]
@@ -131,8 +132,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--c", type=float, default=1.0, help="headline query temperature")
-    ap.add_argument("--sweep", type=str, default="0.0625,0.25,1,4,16,32",
-                    help="extra temperatures reported in 'sweep' (empty: none)")
+    ap.add_argument("--sweep", type=str, default="0.0625,0.25,1,2,4,8,16,32",
+                    help="temperatures reported in 'sweep' at the headline alpha (empty: none)")
+    ap.add_argument("--sweep-alphas", type=str, default="1.25,2",
+                    help="further alphas of the sweep, each at the --sweep-alpha-c temperatures")
+    ap.add_argument("--sweep-alpha-c", type=str, default="1,2,4,8,16,32")
+    ap.add_argument("--long", type=str, default="16384,32768,65536",
+                    help="sequence lengths of the long-context report: B1 H8 d64 bf16 causal, "
+                         "c 16 (empty: none)")
     ap.add_argument("--sweep-steps", type=int, default=5)
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--heads", type=int, default=16)
@@ -338,6 +345,56 @@ def dense_mode_bench(run, steps=5, warmup=2):
             "note": "includes the binding's buffer allocations (torch caching allocator)"}
 
 
+def sweep_point(args, alpha, c):
+    """One point of the sparsity sweep (its own inputs and buffers)."""
+    import torch
+    a = argparse.Namespace(**{**vars(args), "alpha": alpha})
+    r = Runner(a, c)
+    msv, _, _ = r.timed(max(1, args.sweep_steps), 2, per_kernel=False)
+    w = r.work()
+    out = {"alpha": alpha, "c": c, "ms": round(msv, 4),
+           "tflops_dense_equiv": round(w["dense_flops"] / (msv * 1e-3) / 1e12, 3),
+           "tflops_executed": round(sum(w["flops"].values()) / (msv * 1e-3) / 1e12, 3),
+           "block_density": round(w["block_density"], 4),
+           "zero_fraction_sampled": round(r.zero_fraction(), 5),
+           "solver_passes_mean": round(w["passes_mean"], 3)}
+    del r
+    torch.cuda.empty_cache()
+    return out
+
+
+def long_context(args, lengths, steps=3):
+    """The long-context workload (B1 H8 d64 bf16, causal, alpha 1.5, c 16):
+    fwd+bwd time and the device memory it holds, per sequence length."""
+    import torch
+    out = []
+    for n in lengths:
+        a = argparse.Namespace(**{**vars(args), "batch": 1, "heads": 8, "seqlen": n,
+                                  "head_dim": 64, "alpha": 1.5, "causal": True, "steps": steps})
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        r = Runner(a, 16.0)
+        ms, _, _ = r.timed(steps, 1, per_kernel=False)
+        peak = torch.cuda.max_memory_allocated() - base
+        w = r.work()
+        z = r.res.sizes
+        resid = z.tau + z.o2 + z.block_mask + z.q_count + z.q_index + z.k_count + z.k_index + z.stats
+        io = 4 * r.q.numel() * r.q.element_size() + 3 * r.q.numel() * 4  # Q K V dO O, dQ dK dV
+        out.append({"seqlen": n, "ms": round(ms, 3),
+                    "tflops_dense_equiv": round(w["dense_flops"] / (ms * 1e-3) / 1e12, 3),
+                    "tflops_executed": round(sum(w["flops"].values()) / (ms * 1e-3) / 1e12, 3),
+                    "block_density": round(w["block_density"], 4),
+                    "solver_passes_mean": round(w["passes_mean"], 3),
+                    "peak_device_mib": round(peak / 2**20, 1),
+                    "library_residual_mib": round(resid / 2**20, 1),
+                    "library_workspace_mib": round((z.ws_fwd + z.ws_bwd) / 2**20, 1),
+                    "inputs_outputs_mib": round(io / 2**20, 1)})
+        del r
+    torch.cuda.empty_cache()
+    return {"workload": "B1 H8 d64 bf16, causal, alpha 1.5, c 16", "steps": steps, "points": out}
+
+
 def cpu_baseline(runner, heads):
     """The oracle (fp64, all host cores) on `heads` heads of the same workload:
     tau, O, O2, block margins, delta, dQ, dK, dV of every row and column."""
@@ -366,14 +423,14 @@ def main():
         mib = args.calib_copy_mib or 1024
         write_traffic(args.traffic_from[0], args.traffic_from[1], mib,
                       "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run "
-                      "-- python bench.py --steps 2 --warmup 1 --sweep= --no-cpu-baseline "
-                      "--calib-copy-mib %d\n"
+                      "-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-cpu-baseline "
+                      "--no-rows --calib-copy-mib %d\n"
                       "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run "
-                      "-- python bench.py --steps 2 --warmup 1 --sweep= --no-cpu-baseline "
-                      "--calib-copy-mib %d\n"
+                      "-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-cpu-baseline "
+                      "--no-rows --calib-copy-mib %d\n"
                       "python bench.py --traffic-from gpurun_out/pmc_fetch/run_counter_collection.csv "
                       "gpurun_out/pmc_write/run_counter_collection.csv --calib-copy-mib %d"
-                      % (mib, mib, mib))
+                      % (mib, mib, mib), head_dim=args.head_dim)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the alpha-entmax path here is a single-GPU "
@@ -432,22 +489,14 @@ def main():
                      "solver_passes_max": work["passes_max"]},
         "roofline": roofline,
     }
-    sweep = []
-    for cs in [s for s in args.sweep.split(",") if s.strip()]:
-        cval = float(cs)
-        r = Runner(args, cval)
-        msv, _, _ = r.timed(max(1, args.sweep_steps), 2, per_kernel=False)
-        w = r.work()
-        sweep.append({"c": cval, "ms": round(msv, 4),
-                      "tflops_dense_equiv": round(w["dense_flops"] / (msv * 1e-3) / 1e12, 3),
-                      "tflops_executed": round(sum(w["flops"].values()) / (msv * 1e-3) / 1e12, 3),
-                      "block_density": round(w["block_density"], 4),
-                      "zero_fraction_sampled": round(r.zero_fraction(), 5),
-                      "solver_passes_mean": round(w["passes_mean"], 3)})
-        del r
-        torch.cuda.empty_cache()
+    vals = lambda text: [float(x) for x in text.split(",") if x.strip()]
+    sweep = [sweep_point(args, args.alpha, cv) for cv in vals(args.sweep)]
     if sweep:
+        for av in vals(args.sweep_alphas):
+            sweep += [sweep_point(args, av, cv) for cv in vals(args.sweep_alpha_c)]
         out["sweep"] = sweep
+    if args.long.strip():
+        out["long_context"] = long_context(args, [int(x) for x in vals(args.long)])
     if not args.no_rows:
         out["entmax_rows"] = rows_bench()
         out["no_mask_mode"] = dense_mode_bench(run)
