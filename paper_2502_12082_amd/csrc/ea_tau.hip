@@ -198,8 +198,30 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
         float b = m - 1.f;
 #pragma unroll
         for (int j = 1; j < 8; ++j) b = fmaxf(b, fmaf(c, u[j], -exp2f(-__log2f((float)(j + 1)) / g)));
-        // the bound may round above the root by an ulp (constant rows reach it)
-        lo = fminf(b - 1e-6f * fmaxf(1.f, fabsf(b)), hi);
+        // For gamma >= 1, two Newton steps on f restricted to these eight
+        // scores: that f is convex and decreasing, so the steps stay below
+        // its root, which is below tau (the dropped terms are >= 0).  Every z
+        // is at most 1 and z_1 > 0, so the derivative is nonzero.
+        if (g >= 1.f) {
+#pragma unroll
+          for (int it = 0; it < 2; ++it) {
+            float f = -1.f, fp = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              const float z = fmaf(c, u[j], -b);
+              if (z > 0.f) {
+                float pj, uj;
+                Gamma<GK>::pu(z, g, pj, uj);
+                f += pj;
+                fp += uj;
+              }
+            }
+            b += f / (g * fp);
+          }
+        }
+        // the bound may round above the root by a few ulps (rows whose whole
+        // support is among the eight reach it)
+        lo = fminf(b - 4e-6f * fmaxf(1.f, fabsf(b)), hi);
         tau = 0.5f * (lo + hi);
       }
     }
