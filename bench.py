@@ -37,7 +37,7 @@ KERNELS = ("tau_solve", "compact", "fwd_sparse", "bwd_delta", "bwd_dkdv", "bwd_d
 PRODUCTS_PER_ACTIVE = {"fwd_sparse": 3, "bwd_dkdv": 4, "bwd_dq": 3}
 # kernel name fragment in profiler output, and the sources that define each kernel
 PROFILE_NAMES = {"tau_solve": "solve_kernel", "fwd_sparse": "fwd_kernel",
-                 "bwd_dkdv": "dkdv_kernel", "bwd_dq": "dq_kernel"}
+                 "bwd_dkdv": "dkdv2_kernel", "bwd_dq": "dq_kernel"}
 KERNEL_SOURCES = {"tau_solve": ["ea_tau.hip"], "fwd_sparse": ["ea_fwd.hip"],
                   "bwd_dkdv": ["ea_bwd.hip"], "bwd_dq": ["ea_bwd.hip"]}
 COMMON_SOURCES = ["ea_common.h", "ea_internal.h", "../build.py"]

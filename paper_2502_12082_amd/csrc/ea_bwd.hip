@@ -205,6 +205,234 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
   }
 }
 
+// ------------------------------------------------------- dK dV, bf16 inputs
+
+// Eight waves over two adjacent key blocks (2m and 2m + 1).  Wave w owns key
+// block 2m + (w >> 2), key half kh = (w >> 1) & 1 (32 keys, as above) and
+// column half ch = w & 1 of dK and dV.  For each staged query block the wave
+// forms S and dP of its keys against query half ch only, turns them into the
+// operands P, dS_hi and dS_lo of the permuted contractions and posts those
+// through LDS; its partner (same keys, other column half) posts the other
+// query half.  Each wave then accumulates dV and dK for its columns over
+// both query halves.  Half the accumulators and no repeated products let
+// two waves share each SIMD, while every product is formed once.  The two
+// key blocks visit the union of their query-block lists (both ascending);
+// the waves of a key block that does not list the staged query block only
+// keep the barriers.
+constexpr int BWD2_NT = 512;
+
+template <int D, int GK>
+__global__ __launch_bounds__(BWD2_NT, 2) void dkdv2_kernel(BwdArgs a) {
+  using E = __bf16;
+  using TL = Tile<E, D>;
+  using M = Mma<E>;
+  using F = typename M::frag;
+  constexpr int KS = D / M::KW;
+  constexpr int NTH = D / 64;  // 32-column output tiles per wave
+  constexpr int PS = perm_steps<E>();
+  __shared__ __attribute__((aligned(16))) E qbuf[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) E dobuf[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) float tau_s[2][BLK];
+  __shared__ __attribute__((aligned(16))) float del_s[2][BLK];
+  // operands posted by each wave: [wave][P, dS hi, dS lo][step][lane]
+  __shared__ __attribute__((aligned(16))) u32x4 post[BWD2_NT / 64][3][PS][64];
+
+  const int lane = lane_id(), w = wave_id();
+  const int kh = (w >> 1) & 1, ch = w & 1;
+  const int n = a.n, T = a.T;
+  const int bh = blockIdx.x % a.BH;
+  const int kbA = 2 * (blockIdx.x / a.BH);  // causal: small key blocks have the longest lists
+  const int kbB = kbA + 1;
+  const bool mineA = (w >> 2) == 0;
+  const int k0 = (mineA ? kbA : kbB) * BLK + 32 * kh;
+  const int j = k0 + (lane & 31);
+  const bool wave_ok = k0 < n;
+  const size_t head = (size_t)bh * n * D;
+  const E* Qg = static_cast<const E*>(a.q) + head;
+  const E* Kg = static_cast<const E*>(a.k) + head;
+  const E* Vg = static_cast<const E*>(a.v) + head;
+  const E* dOg = static_cast<const E*>(a.dout) + head;
+  const float* taug = a.tau + (size_t)bh * n;
+  const float* delg = a.delta + (size_t)bh * n;
+  const float c = a.c, g = a.gamma;
+
+  F kf[KS], vf[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    kf[kk] = load_row_frag_global<E, D>(Kg, j, n, kk);
+    vf[kk] = load_row_frag_global<E, D>(Vg, j, n, kk);
+  }
+
+  // Query-block lists of the two key blocks (without tables, in the no-mask
+  // mode, every valid query block), merged in ascending order.
+  const bool dense = a.k_index == nullptr;
+  auto count_of = [&](int kb) {
+    if (kb >= T) return 0;
+    return dense ? (a.causal ? T - kb : T) : a.k_count[(size_t)bh * T + kb];
+  };
+  auto entry_of = [&](int kb, int e) {
+    return dense ? (a.causal ? kb + e : e) : a.k_index[((size_t)bh * T + kb) * T + e];
+  };
+  const int nA = count_of(kbA), nB = count_of(kbB);
+  int pA = 0, pB = 0;
+  // the next query block of the union, and whether each key block lists it
+  auto next = [&](int& qb, bool& inA, bool& inB) {
+    const int hA = pA < nA ? entry_of(kbA, pA) : T;
+    const int hB = pB < nB ? entry_of(kbB, pB) : T;
+    qb = min(hA, hB);
+    inA = hA == qb;
+    inB = hB == qb;
+    pA += inA ? 1 : 0;
+    pB += inB ? 1 : 0;
+    return qb < T;
+  };
+
+  f32x16 dk[NTH], dv[NTH];
+#pragma unroll
+  for (int t = 0; t < NTH; ++t) {
+    dk[t] = zero16();
+    dv[t] = zero16();
+  }
+
+  // S = Q K^T, dP = dO V^T of query half qh (rows = queries) for this wave's
+  // keys; masked sub-tiles set invalid scores to -inf (then P = dS = 0).
+  auto operands = [&](const E* qt, const E* dt, const float* ts, const float* ds_, int qh,
+                      bool masked, int i0, F* pa, F* dh, F* dl) {
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      s = M::mma(lds_row_frag<E, D>(qt, 32 * qh + (lane & 31), kk), kf[kk], s);
+      dp = M::mma(lds_row_frag<E, D>(dt, 32 * qh + (lane & 31), kk), vf[kk], dp);
+    }
+    if (masked) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = i0 + crow(r);
+        if (!(i < n && j < n && (!a.causal || j <= i))) s[r] = -INFINITY;
+      }
+    }
+    float p[16], dsv[16];
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const int q4 = 32 * qh + 8 * g4 + 4 * (lane >> 5);
+      const f32x4 tq = *reinterpret_cast<const f32x4*>(ts + q4);
+      const f32x4 dq4 = *reinterpret_cast<const f32x4*>(ds_ + q4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * g4 + e;
+        const float zp = relu_z(c, s[r], tq[e]);
+        float u;
+        Gamma<GK>::pu(zp, g, p[r], u);
+        dsv[r] = u * (dp[r] - dq4[e]);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < PS; ++t) {
+      pa[t] = M::pack(p, t);
+      M::pack_split(dsv, t, dh[t], dl[t]);
+    }
+  };
+  // dV += P^T dO and dK += dS^T Q over query half qh, this wave's columns
+  auto accum = [&](const E* qt, const E* dt, int qh, const F* pa, const F* dh, const F* dl) {
+#pragma unroll
+    for (int t = 0; t < PS; ++t) {
+#pragma unroll
+      for (int nt = 0; nt < NTH; ++nt) {
+        const int col0 = 32 * (ch * NTH + nt);
+        dv[nt] = M::mma(pa[t], lds_perm_frag<E, D>(dt, col0, 32 * qh, t), dv[nt]);
+        const F qb_ = lds_perm_frag<E, D>(qt, col0, 32 * qh, t);
+        dk[nt] = M::mma(dh[t], qb_, dk[nt]);
+        dk[nt] = M::mma(dl[t], qb_, dk[nt]);
+      }
+    }
+  };
+  auto half_valid = [&](int i0) { return !(i0 >= n || (a.causal && k0 > i0 + 31)); };
+  auto half_masked = [&](int i0) {
+    return i0 + 31 >= n || k0 + 31 >= n || (a.causal && k0 + 31 > i0);
+  };
+
+  float tv = 0.f, dlv = 0.f;
+  DmaPlan<E, D, BWD2_NT> dma;
+  dma.init();
+  auto issue = [&](int qb, int b) {
+    dma.issue(qbuf[b], Qg, qb * BLK, n);
+    dma.issue(dobuf[b], dOg, qb * BLK, n);
+    if (threadIdx.x < BLK) {
+      const int r = min(qb * BLK + (int)threadIdx.x, n - 1);
+      tv = taug[r];
+      dlv = delg[r];
+    }
+  };
+  // S, dP, P, dS of query half ch (kept for this wave, posted for its partner)
+  F pa[PS], dh[PS], dl[PS];
+  auto phase1 = [&](int qb, int b, int tb) {
+    const int i0 = qb * BLK + 32 * ch;
+    if (!half_valid(i0)) return;
+    operands(qbuf[b], dobuf[b], tau_s[tb], del_s[tb], ch, half_masked(i0), i0, pa, dh, dl);
+#pragma unroll
+    for (int t = 0; t < PS; ++t) {
+      post[w][0][t][lane] = __builtin_bit_cast(u32x4, pa[t]);
+      post[w][1][t][lane] = __builtin_bit_cast(u32x4, dh[t]);
+      post[w][2][t][lane] = __builtin_bit_cast(u32x4, dl[t]);
+    }
+  };
+  // both query halves into this wave's columns: the partner's half first
+  auto phase2 = [&](int qb, int b) {
+    if (half_valid(qb * BLK + 32 * (ch ^ 1))) {
+      F xa[PS], xh[PS], xl[PS];
+#pragma unroll
+      for (int t = 0; t < PS; ++t) {
+        xa[t] = __builtin_bit_cast(F, post[w ^ 1][0][t][lane]);
+        xh[t] = __builtin_bit_cast(F, post[w ^ 1][1][t][lane]);
+        xl[t] = __builtin_bit_cast(F, post[w ^ 1][2][t][lane]);
+      }
+      accum(qbuf[b], dobuf[b], ch ^ 1, xa, xh, xl);
+    }
+    if (half_valid(qb * BLK + 32 * ch)) accum(qbuf[b], dobuf[b], ch, pa, dh, dl);
+  };
+
+  int qc = 0;
+  bool inA = false, inB = false;
+  bool have = next(qc, inA, inB);
+  if (have) issue(qc, 0);
+  for (int b = 0; have; b ^= 1) {
+    int qn = 0;
+    bool nA_ = false, nB_ = false;
+    const bool more = next(qn, nA_, nB_);
+    dma_wait();
+    if (threadIdx.x < BLK) {
+      tau_s[b][threadIdx.x] = tv;
+      del_s[b][threadIdx.x] = dlv;
+    }
+    __syncthreads();  // block qc is staged; every wave is done with the previous one
+    if (more) issue(qn, b ^ 1);
+    const bool act = wave_ok && (mineA ? inA : inB);
+    if (act) phase1(qc, b, b);
+    __syncthreads();  // the posted operands are visible
+    if (act) phase2(qc, b);
+    qc = qn;
+    inA = nA_;
+    inB = nB_;
+    have = more;
+  }
+
+  if (!wave_ok) return;
+  float* dK = a.dk + head;
+  float* dV = a.dv + head;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int key = k0 + crow(r);
+    if (key < n) {
+#pragma unroll
+      for (int nt = 0; nt < NTH; ++nt) {
+        const size_t off = (size_t)key * D + 32 * (ch * NTH + nt) + (lane & 31);
+        dK[off] = a.scale * dk[nt][r];
+        dV[off] = dv[nt][r];
+      }
+    }
+  }
+}
+
 // --------------------------------------------------------------------- dQ
 
 constexpr int DQ_NT = 256;
@@ -346,6 +574,14 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
 
 template <typename E, int D>
 hipError_t launch_dkdv_d(const BwdArgs& a, hipStream_t s) {
+  if constexpr (sizeof(E) == 2) {
+    dim3 grid((unsigned)(a.BH * ((a.T + 1) / 2))), block(BWD2_NT);
+    auto kernel = dkdv2_kernel<D, 0>;
+    if (a.gk == 1) kernel = dkdv2_kernel<D, 1>;
+    if (a.gk == 2) kernel = dkdv2_kernel<D, 2>;
+    if (a.gk == 4) kernel = dkdv2_kernel<D, 4>;
+    return launch_kernel(kernel, grid, block, s, a);
+  }
   dim3 grid((unsigned)(a.BH * a.T)), block(BWD_NT);
   auto kernel = dkdv_kernel<E, D, 0>;
   if (a.gk == 1) kernel = dkdv_kernel<E, D, 1>;
