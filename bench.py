@@ -75,6 +75,16 @@ def measured_traffic(kernel):
     return float(fields["hbm_bytes_per_launch"])
 
 
+def headline_instance(name, head_dim):
+    """Whether a profiled kernel name is a bf16 instantiation for head_dim.
+    rocprofv3 prints names with a __bf16 template argument mangled (dtype
+    "DF16b", fp32 "If", head_dim "Li<d>E") and the bf16-only kernels'
+    demangled ("dkdv2_kernel<128, 2>")."""
+    if name.startswith("_Z"):
+        return ("Li%dE" % head_dim) in name and "IfLi" not in name
+    return ("<%d," % head_dim) in name or ("__bf16, %d," % head_dim) in name
+
+
 def write_traffic(fetch_csv, write_csv, calib_mib, command, head_dim=128):
     """Scale each kernel's FETCH_SIZE and WRITE_SIZE (KiB per dispatch) by what
     the same counter reads for the plain copy of `calib_mib` MiB, and write
@@ -101,7 +111,7 @@ def write_traffic(fetch_csv, write_csv, calib_mib, command, head_dim=128):
     f_scale = calib_kib / max(fetch[cname])
     w_scale = calib_kib / max(write[cname])
     for kernel, frag in PROFILE_NAMES.items():
-        names = [k for k in fetch if frag in k and ("DF16bLi%dE" % head_dim) in k]
+        names = [k for k in fetch if frag in k and headline_instance(k, head_dim)]
         if not names:
             continue
         fk = [v for k in names for v in fetch[k]]
