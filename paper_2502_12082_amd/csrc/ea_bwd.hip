@@ -574,7 +574,10 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
 
 template <typename E, int D>
 hipError_t launch_dkdv_d(const BwdArgs& a, hipStream_t s) {
-  if constexpr (sizeof(E) == 2) {
+  // d = 128 bf16 takes the column-split kernel; at d = 64 (and for fp32)
+  // the one-block kernel already runs two waves per SIMD without the union
+  // of two query-block lists, and is faster on sparse masks.
+  if constexpr (sizeof(E) == 2 && D == 128) {
     dim3 grid((unsigned)(a.BH * ((a.T + 1) / 2))), block(BWD2_NT);
     auto kernel = dkdv2_kernel<D, 0>;
     if (a.gk == 1) kernel = dkdv2_kernel<D, 1>;
