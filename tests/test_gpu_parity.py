@@ -80,7 +80,7 @@ def test_decoder_step():
 
 
 def _sampled_case(B, H, n, d, alpha, causal, c, block_rows, ncols, heads, label,
-                  full_cols=False):
+                  full_cols=False, col_blocks=None):
     inp = synth.attention_inputs(B, H, n, d, c=c, dtype="bf16", with_dout=True,
                                  seed=synth.SEED_BASE)
     scale = d ** -0.5
@@ -89,6 +89,8 @@ def _sampled_case(B, H, n, d, alpha, causal, c, block_rows, ncols, heads, label,
     T = (n + 63) // 64
     rows = sorted(set(r for I in block_rows for r in range(I * 64, min(n, I * 64 + 64))))
     cols = list(range(n - ncols, n)) if ncols else None
+    if col_blocks:
+        cols = sorted(set(j for J in col_blocks for j in range(J * 64, min(n, J * 64 + 64))))
     out = []
     for bh in heads:
         ref = oracle_head(inp, bh, alpha, scale, causal, True, rows=rows, cols=cols,
@@ -116,6 +118,21 @@ def test_sweep_workload_full_head():
     check_tables(gpu, False)
     ref = oracle_head(inp, 5, 1.5, 128 ** -0.5, False, True)
     log("  errors %s" % check_head(gpu, ref, 5, "bf16", "sweep-full"))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_dkdv_sparse_key_block_pairs(causal):
+    """bf16 d128 at a sparse mask (c = 32): dK and dV of the key blocks of
+    several adjacent pairs, whose query-block lists differ; the d = 128 dK/dV
+    kernel walks the union of each pair's lists."""
+    n = 4096
+    gpu, _ = _sampled_case(1, 2, n, 128, 1.5, causal, 32.0, block_rows=[0, 63], ncols=0,
+                           heads=[0, 1], label="pairs", col_blocks=[0, 1, 20, 21, 62, 63])
+    kc = gpu["k_count"][0]
+    ki = gpu["k_index"][0]
+    differ = [m for m in (0, 10, 31) if kc[2 * m] != kc[2 * m + 1]
+              or not np.array_equal(ki[2 * m, :kc[2 * m]], ki[2 * m + 1, :kc[2 * m + 1]])]
+    assert differ, "the chosen pairs should have different query-block lists"
 
 
 @pytest.mark.parametrize("n", [16384, 65536])
