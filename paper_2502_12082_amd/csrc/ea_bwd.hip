@@ -219,6 +219,11 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
 // key blocks visit the union of their query-block lists (both ascending);
 // the waves of a key block that does not list the staged query block only
 // keep the barriers.
+//
+// The Q and dO tiles (with their tau and delta) go through three LDS stages,
+// so each copy has two steps to land, and the barriers wait only for LDS
+// traffic: a plain workgroup barrier would also wait for the copies in
+// flight.  The tables are read by scalar loads for the same reason.
 constexpr int BWD2_NT = 512;
 
 template <int D, int GK>
@@ -230,10 +235,11 @@ __global__ __launch_bounds__(BWD2_NT, 2) void dkdv2_kernel(BwdArgs a) {
   constexpr int KS = D / M::KW;
   constexpr int NTH = D / 64;  // 32-column output tiles per wave
   constexpr int PS = perm_steps<E>();
-  __shared__ __attribute__((aligned(16))) E qbuf[2][TL::ELEMS];
-  __shared__ __attribute__((aligned(16))) E dobuf[2][TL::ELEMS];
-  __shared__ __attribute__((aligned(16))) float tau_s[2][BLK];
-  __shared__ __attribute__((aligned(16))) float del_s[2][BLK];
+  // three stages: block e is read while e + 1 and e + 2 are in flight
+  __shared__ __attribute__((aligned(16))) E qbuf[3][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) E dobuf[3][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) float tau_s[3][BLK];
+  __shared__ __attribute__((aligned(16))) float del_s[3][BLK];
   // operands posted by each wave: [wave][P, dS hi, dS lo][step][lane]
   __shared__ __attribute__((aligned(16))) u32x4 post[BWD2_NT / 64][3][PS][64];
 
@@ -252,8 +258,8 @@ __global__ __launch_bounds__(BWD2_NT, 2) void dkdv2_kernel(BwdArgs a) {
   const E* Kg = static_cast<const E*>(a.k) + head;
   const E* Vg = static_cast<const E*>(a.v) + head;
   const E* dOg = static_cast<const E*>(a.dout) + head;
-  const float* taug = a.tau + (size_t)bh * n;
-  const float* delg = a.delta + (size_t)bh * n;
+  [[maybe_unused]] const float* taug = a.tau + (size_t)bh * n;  // read by tile copies
+  [[maybe_unused]] const float* delg = a.delta + (size_t)bh * n;
   const float c = a.c, g = a.gamma;
 
   F kf[KS], vf[KS];
@@ -266,12 +272,17 @@ __global__ __launch_bounds__(BWD2_NT, 2) void dkdv2_kernel(BwdArgs a) {
   // Query-block lists of the two key blocks (without tables, in the no-mask
   // mode, every valid query block), merged in ascending order.
   const bool dense = a.k_index == nullptr;
+  // The tables are read through the constant address space (scalar loads),
+  // so that reading them does not wait on the tile copies in flight.
+  typedef const __attribute__((address_space(4))) int32_t ci32;
+  const ci32* kcount = (const ci32*)a.k_count;
+  const ci32* kindex = (const ci32*)a.k_index;
   auto count_of = [&](int kb) {
     if (kb >= T) return 0;
-    return dense ? (a.causal ? T - kb : T) : a.k_count[(size_t)bh * T + kb];
+    return dense ? (a.causal ? T - kb : T) : kcount[(size_t)bh * T + kb];
   };
   auto entry_of = [&](int kb, int e) {
-    return dense ? (a.causal ? kb + e : e) : a.k_index[((size_t)bh * T + kb) * T + e];
+    return dense ? (a.causal ? kb + e : e) : kindex[((size_t)bh * T + kb) * T + e];
   };
   const int nA = count_of(kbA), nB = count_of(kbB);
   int pA = 0, pB = 0;
@@ -351,16 +362,35 @@ __global__ __launch_bounds__(BWD2_NT, 2) void dkdv2_kernel(BwdArgs a) {
     return i0 + 31 >= n || k0 + 31 >= n || (a.causal && k0 + 31 > i0);
   };
 
-  float tv = 0.f, dlv = 0.f;
-  DmaPlan<E, D, BWD2_NT> dma;
+  using Plan = DmaPlan<E, D, BWD2_NT>;
+  static_assert(Plan::NI % Plan::NW == 0 && 2 * Plan::PER + 2 <= 15, "copy counts");
+  Plan dma;
   dma.init();
+  // Copies of query block qb into stage b: the Q and dO tiles, and (wave 0)
+  // its tau and delta values, all by global_load_lds.
   auto issue = [&](int qb, int b) {
     dma.issue(qbuf[b], Qg, qb * BLK, n);
     dma.issue(dobuf[b], dOg, qb * BLK, n);
-    if (threadIdx.x < BLK) {
-      const int r = min(qb * BLK + (int)threadIdx.x, n - 1);
-      tv = taug[r];
-      dlv = delg[r];
+#if defined(__HIP_DEVICE_COMPILE__)
+    if (w == 0) {
+      const int r = min(qb * BLK + lane, n - 1);
+      __builtin_amdgcn_global_load_lds(taug + r, to_lds(&tau_s[b][0]), 4, 0, 0);
+      __builtin_amdgcn_global_load_lds(delg + r, to_lds(&del_s[b][0]), 4, 0, 0);
+    }
+#endif
+  };
+  // Workgroup barrier for LDS traffic only: this wave's LDS operations
+  // complete first, but copies still in flight are not waited for (the
+  // plain barrier would also wait for every global load, so the next
+  // stages' copies would have to land first).
+  auto lds_barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+  // Waits until every copy but those of the latest issue has landed (the
+  // counter completes in issue order; wave 0 issues two more per stage).
+  auto wait_all_but_latest = [&]() {
+    if (w == 0) {
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * Plan::PER + 2));
+    } else {
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * Plan::PER));
     }
   };
   // S, dP, P, dS of query half ch (kept for this wave, posted for its partner)
@@ -391,29 +421,40 @@ __global__ __launch_bounds__(BWD2_NT, 2) void dkdv2_kernel(BwdArgs a) {
     if (half_valid(qb * BLK + 32 * ch)) accum(qbuf[b], dobuf[b], ch, pa, dh, dl);
   };
 
-  int qc = 0;
-  bool inA = false, inB = false;
-  bool have = next(qc, inA, inB);
-  if (have) issue(qc, 0);
-  for (int b = 0; have; b ^= 1) {
-    int qn = 0;
-    bool nA_ = false, nB_ = false;
-    const bool more = next(qn, nA_, nB_);
-    dma_wait();
-    if (threadIdx.x < BLK) {
-      tau_s[b][threadIdx.x] = tv;
-      del_s[b][threadIdx.x] = dlv;
+  // Union entries e (stage b0), e + 1 and e + 2 (in flight).
+  int q0 = 0, q1 = 0;
+  bool a0 = false, b0_ = false, a1 = false, b1_ = false;
+  bool h0 = next(q0, a0, b0_);
+  bool h1 = h0 && next(q1, a1, b1_);
+  if (h0) issue(q0, 0);
+  if (h1) issue(q1, 1);
+  int st = 0;
+  while (h0) {
+    int q2 = 0;
+    bool a2 = false, b2_ = false;
+    const bool h2 = h1 && next(q2, a2, b2_);
+    if (h1) {
+      wait_all_but_latest();
+    } else {
+      dma_wait();
     }
-    __syncthreads();  // block qc is staged; every wave is done with the previous one
-    if (more) issue(qn, b ^ 1);
-    const bool act = wave_ok && (mineA ? inA : inB);
-    if (act) phase1(qc, b, b);
-    __syncthreads();  // the posted operands are visible
-    if (act) phase2(qc, b);
-    qc = qn;
-    inA = nA_;
-    inB = nB_;
-    have = more;
+    // block q0 is staged (each wave waited for its own copies); every wave
+    // is done with the previous step, whose stage receives block q2
+    lds_barrier();
+    if (h2) issue(q2, st == 0 ? 2 : st - 1);
+    const bool act = wave_ok && (mineA ? a0 : b0_);
+    if (act) phase1(q0, st, st);
+    lds_barrier();  // the posted operands are visible
+    if (act) phase2(q0, st);
+    q0 = q1;
+    a0 = a1;
+    b0_ = b1_;
+    h0 = h1;
+    q1 = q2;
+    a1 = a2;
+    b1_ = b2_;
+    h1 = h2;
+    st = st == 2 ? 0 : st + 1;
   }
 
   if (!wave_ok) return;
