@@ -111,8 +111,9 @@ ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_s
  *            tiles).  A tile with a slot stores, while it finds the row
  *            maxima, the scores above each row's lower bracket end and runs
  *            its evaluations on them instead of streaming K again (when the
- *            stored scores do not fit, it streams K, and tries once more
- *            after its brackets have narrowed); tiles without one (all of
+ *            stored scores do not fit, it streams K, and collects once more
+ *            if its first streamed evaluation counts few enough scores above
+ *            the lower end); tiles without one (all of
  *            them for NULL) stream K on every pass.  Results agree up to
  *            rounding either way.  Contents are scratch.
  * Launches 3 kernels on `stream`.

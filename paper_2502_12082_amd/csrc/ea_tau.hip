@@ -875,6 +875,9 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     }
   }
   stream([&](int kb, const E* kt) {
+    // once the lists have overflowed, the first stream's blocks need nothing
+    // more (their maxima are in)
+    if (kb < W && fill_dead) return;
     f32x16 s[2][2];
     int k[2][2];
     if (!block(kb, kt, s, k)) return;
@@ -960,7 +963,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     for (int gq = 0; gq < 2; ++gq) cmax[gq] = wave_max(cc[gq]);
   }
   int attempts = cache ? 1 : 0;  // cache fills tried (pass 0 is the first)
-  bool small_support = false;    // every list's support count <= cap / 2
+  bool fits = false;             // a fill at the current lower end would fit
   float f_prev[2] = {INFINITY, INFINITY};
 
   for (int it = 0;; ++it) {
@@ -1051,9 +1054,10 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     };
 
     // If the lists of pass 0 overflowed, collecting them is tried once more
-    // in a K pass of its own, once the last streamed evaluation suggests
-    // that they fit (the brackets have narrowed by then).
-    if (!cached && cache && it >= 1 && attempts < 2 && small_support) {
+    // in a K pass of its own, when the first streamed evaluation counted few
+    // enough scores above its lower end: the fill keeps the scores above the
+    // lower end as it stands now, which has only risen since, so it fits.
+    if (!cached && cache && it >= 1 && attempts < 2 && fits) {
       ++attempts;
       cc[0] = cc[1] = 0;
       stream([&](int kb, const E* kt) {
@@ -1070,7 +1074,11 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       fill_done();
     }
     if (!cached) {
-      // streamed evaluation; the mask bits of every block are rewritten
+      // streamed evaluation; the mask bits of every block are rewritten.  The
+      // first one after an overflow also counts the scores above the lower
+      // end, the size of a fill at this point.
+      const bool count = cache && attempts < 2;
+      int over[2] = {0, 0};
       uint32_t word = 0;  // mask bits of the current 32-block group (wave-uniform)
       stream([&](int kb, const E* kt) {
         f32x16 s[2][2];
@@ -1081,7 +1089,13 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
           for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int gq = 0; gq < 2; ++gq)
-              if (k[h][gq]) any |= eval_tile(s[h][gq], gq);
+              if (k[h][gq]) {
+                any |= eval_tile(s[h][gq], gq);
+                if (count) {
+#pragma unroll
+                  for (int r = 0; r < 16; ++r) over[gq] += s[h][gq][r] > s_lo[gq] ? 1 : 0;
+                }
+              }
         }
         if (__ballot(any) != 0ull) word |= 1u << (kb & 31);
         if ((kb & 31) == 31 || kb == nkb - 1) {
@@ -1090,7 +1104,10 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         }
       });
       ++passes;
-      small_support = !__syncthreads_or(mc[0] > a.cap / 2 || mc[1] > a.cap / 2);
+      if (count) {
+        fits = !__syncthreads_or(over[0] > a.cap || over[1] > a.cap);
+        if (!fits) attempts = 2;  // no retry, and no more counting
+      }
     } else {
 #pragma unroll
       for (int gq = 0; gq < 2; ++gq)
