@@ -158,6 +158,8 @@ def parse():
     ap.add_argument("--alpha", type=float, default=1.5)
     ap.add_argument("--causal", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the tiny, encoder and decoder workloads")
     ap.add_argument("--cpu-heads", type=int, default=4, help="heads in the oracle sample")
     ap.add_argument("--no-rows", action="store_true",
                     help="skip the row-wise entmax measurement (materialized 8192 x 8192 scores)")
@@ -173,19 +175,23 @@ def parse():
 class Runner:
     """Device buffers and the six stage launches of one configuration."""
 
-    def __init__(self, args, c):
+    def __init__(self, args, c, dtype="bf16", bwd=True):
         import torch
         import synth
         import paper_2502_12082_amd as ea
         self.ea, self.torch = ea, torch
         B, H, n, d = args.batch, args.heads, args.seqlen, args.head_dim
         self.B, self.H, self.n, self.d, self.c = B, H, n, d, c
-        inp = synth.attention_inputs(B, H, n, d, c=c, dtype="bf16", with_dout=True)
+        self.bwd = bwd
+        inp = synth.attention_inputs(B, H, n, d, c=c, dtype=dtype, with_dout=True)
         self.inp = inp
-        dev = lambda t: torch.from_numpy(t.raw.view(np.int16)).view(torch.bfloat16).cuda()
+        if dtype == "bf16":
+            dev = lambda t: torch.from_numpy(t.raw.view(np.int16)).view(torch.bfloat16).cuda()
+        else:
+            dev = lambda t: torch.from_numpy(np.ascontiguousarray(t.raw, dtype=np.float32)).cuda()
         self.q, self.k, self.v, self.do = (dev(inp[x]) for x in ("q", "k", "v", "dout"))
         self.shape = ea.make_shape(self.q)
-        self.params = ea.make_params(args.alpha, d ** -0.5, args.causal, True, head_dim=d)
+        self.params = ea.make_params(args.alpha, d ** -0.5, args.causal, bwd, head_dim=d)
         self.res = ea.Residuals(self.shape, self.params, self.q.device)
         self.rp = self.res.ptrs()
         self.o = torch.empty_like(self.q)
@@ -208,6 +214,8 @@ class Runner:
                                                self.ws_fwd.numel(), s), "fwd stage")
             if ev:
                 ev[1 + st].record()
+        if not self.bwd:
+            return
         for st in range(3):
             ea._check(ea.entmax_attn_bwd_stage(st, self.shape, self.params, q, k, v, do, self.rp,
                                                self.dq.data_ptr(), self.dk.data_ptr(),
@@ -373,6 +381,35 @@ def sweep_point(args, alpha, c):
     return out
 
 
+def other_configs(args, steps=5):
+    """The other workload shapes, each at its own size: the tiny fp32 forward,
+    the encoder-shaped forward at three temperatures and the decoder-shaped
+    training step (ms per call and dense-equivalent TFLOP/s)."""
+    import torch
+    cases = [("tiny forward", 1, 1, 256, 64, "f32", False, 1.0, False),
+             ("encoder forward", 8, 12, 1024, 64, "bf16", False, 1.0, False),
+             ("encoder forward", 8, 12, 1024, 64, "bf16", False, 4.0, False),
+             ("encoder forward", 8, 12, 1024, 64, "bf16", False, 16.0, False),
+             ("decoder step", 4, 12, 4096, 64, "bf16", True, 8.0, True)]
+    out = []
+    for name, B, H, n, d, dt, causal, c, bwd in cases:
+        a = argparse.Namespace(**{**vars(args), "batch": B, "heads": H, "seqlen": n,
+                                  "head_dim": d, "alpha": 1.5, "causal": causal, "steps": steps})
+        r = Runner(a, c, dtype=dt, bwd=bwd)
+        ms, _, _ = r.timed(steps, 2, per_kernel=False)
+        w = r.work()
+        flops = (14.0 if bwd else 4.0) * n * n * d * B * H * (0.5 if causal else 1.0)
+        out.append({"config": name, "shape": "B%d H%d n%d d%d %s%s" % (
+                        B, H, n, d, dt, " causal" if causal else ""),
+                    "c": c, "fwd_bwd" if bwd else "fwd": True, "ms": round(ms, 4),
+                    "tflops_dense_equiv": round(flops / (ms * 1e-3) / 1e12, 3),
+                    "block_density": round(w["block_density"], 4),
+                    "solver_passes_mean": round(w["passes_mean"], 3)})
+        del r
+        torch.cuda.empty_cache()
+    return out
+
+
 def long_context(args, lengths, steps=3):
     """The long-context workload (B1 H8 d64 bf16, causal, alpha 1.5, c 16):
     fwd+bwd time and the device memory it holds, per sequence length."""
@@ -433,10 +470,10 @@ def main():
         mib = args.calib_copy_mib or 1024
         write_traffic(args.traffic_from[0], args.traffic_from[1], mib,
                       "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run "
-                      "-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-cpu-baseline "
+                      "-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-configs --no-cpu-baseline "
                       "--no-rows --calib-copy-mib %d\n"
                       "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run "
-                      "-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-cpu-baseline "
+                      "-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-configs --no-cpu-baseline "
                       "--no-rows --calib-copy-mib %d\n"
                       "python bench.py --traffic-from gpurun_out/pmc_fetch/run_counter_collection.csv "
                       "gpurun_out/pmc_write/run_counter_collection.csv --calib-copy-mib %d"
@@ -507,6 +544,8 @@ def main():
         out["sweep"] = sweep
     if args.long.strip():
         out["long_context"] = long_context(args, [int(x) for x in vals(args.long)])
+    if not args.no_configs:
+        out["other_configs"] = other_configs(args)
     if not args.no_rows:
         out["entmax_rows"] = rows_bench()
         out["no_mask_mode"] = dense_mode_bench(run)
