@@ -24,7 +24,7 @@ constexpr int MAX_ITER_CAP = 64;
 // Candidate-cache entries per list (see entmax_attn_sizes); a slot holds
 // two lists per row of a workgroup.
 constexpr int TAU_CACHE_CAP = 192;
-static_assert(TAU_CACHE_CAP % 8 == 0, "the solver reads lists in batches of 8 entries");
+static_assert(TAU_CACHE_CAP % 16 == 0, "the solver reads lists in batches of 16 entries");
 constexpr size_t SOLVE_SLOT_BYTES = (size_t)TAU_CACHE_CAP * 2 * SOLVE_ROWS * sizeof(CandEntry);
 constexpr size_t TAU_SLOT_BYTES = (size_t)TAU_CACHE_CAP * 2 * TAU_ROWS * sizeof(CandEntry);
 

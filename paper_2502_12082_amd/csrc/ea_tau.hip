@@ -836,7 +836,25 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         if (e0 + u < cc[gq]) use(ce[u].s, ce[u].kb);
     }
   };
-  auto scan = [&](int gq, auto&& use) { scan_kb(gq, [&](float sv, int) { use(sv); }); };
+  // The scores of both lists for an evaluation: sixteen independent 4-byte
+  // loads from each list per batch, up to the longer wave maximum rounded up
+  // to 16 (inside the slot: cap is a multiple of 16).  use(gq, score).
+  auto scan_scores = [&](auto&& use) {
+    const int m = max(cmax[0], cmax[1]);
+    for (int e0 = 0; e0 < m; e0 += 16) {
+      float v0[16], v1[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        v0[u] = cache[entry_idx(e0 + u, 0)].s;
+        v1[u] = cache[entry_idx(e0 + u, 1)].s;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        if (e0 + u < cc[0]) use(0, v0[u]);
+        if (e0 + u < cc[1]) use(1, v1[u]);
+      }
+    }
+  };
   // Keeps the entries of list gq above `sb` (all lanes of the wave).
   auto filter = [&](int gq, float sb) {
     cmax[gq] = wave_max(cc[gq]);
@@ -1109,9 +1127,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         if (!fits) attempts = 2;  // no retry, and no more counting
       }
     } else {
-#pragma unroll
-      for (int gq = 0; gq < 2; ++gq)
-        scan(gq, [&](float sv) { add_z(relu_z(c, sv, tau[gq]), gq); });
+      scan_scores([&](int gq, float sv) { add_z(relu_z(c, sv, tau[gq]), gq); });
     }
 
     bool conv = true;
