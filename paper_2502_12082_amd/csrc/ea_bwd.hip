@@ -17,12 +17,15 @@
 // rounded to bf16 for P^T dO; dS is fed to the MFMA as a two-term bf16 split
 // (hi + lo) so dK and dQ keep ~16 mantissa bits of dS; outputs are fp32.
 //
-// gfx950 layout: 2 waves per workgroup, 32 resident rows per wave in
-// registers (K and V rows for dK/dV; Q and dO rows for dQ); the other side's
-// 64-row tiles are copied by global_load_lds into double-buffered row-major
-// LDS tiles, read directly for S and dP and through transposing LDS reads for
-// the permuted contractions P^T dO, dS^T Q and dS K.  No atomics: every
-// output row has one owner, so results are deterministic.
+// gfx950 layout: 32 resident rows per wave in registers (K and V rows for
+// dK/dV; Q and dO rows for dQ); the other side's 64-row tiles are copied by
+// global_load_lds into row-major LDS tiles (two stages; three in the bf16
+// d = 128 dK/dV kernel), read directly for S and dP and through transposing
+// LDS reads for the permuted contractions P^T dO, dS^T Q and dS K.  The dK/dV
+// work has two forms: dkdv_kernel (2 waves per key block, every column) and,
+// for bf16 at d = 128, dkdv2_kernel (8 waves over two key blocks, each wave
+// half of the columns, S and dP operands shared through LDS).  No atomics:
+// every output row has one owner, so results are deterministic.
 #include <type_traits>
 
 #include "ea_common.h"
