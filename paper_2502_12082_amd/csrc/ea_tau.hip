@@ -916,8 +916,9 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     if (!cache || fill_dead) return;
     // Every 4 blocks the running bound takes the one-term bound of the
     // current maxima, every 32 blocks the Newton-refined one (any valid
-    // lower bound serves; the first stream already left a close one).
-    if ((kb & 3) == 0) {
+    // lower bound serves; the first stream already left a close one).  The
+    // maxima only change from block W on.
+    if (kb >= W && (kb & 3) == 0) {
 #pragma unroll
       for (int gq = 0; gq < 2; ++gq) {
         float u[8];
