@@ -13,14 +13,14 @@
 // O2_i = U V / sum U (the O^(2) of App. A.2).  O is not renormalised: the
 // row sums are 1 + f(tau) of the returned tau (Algorithm 1 output).
 //
-// gfx950 layout: one workgroup = 2 waves = one 64-row query block; each wave
-// holds 32 query rows as MFMA B operands, computes S^T (keys x queries) so the
-// probabilities come out with one query per lane, and feeds them back as the
-// A operand of P V with a permuted contraction order (see ea_common.h).  K and
-// V blocks are copied into double-buffered LDS tiles by global_load_lds (the
-// next listed block in flight while the current one is consumed); V's
-// operand fragments come out of its row-major tile through transposing LDS
-// reads.
+// gfx950 layout: one workgroup = 4 waves = one 64-row query block; each wave
+// holds 32 query rows as MFMA B operands and takes one 32-key half of every
+// listed key block, computes S^T (keys x queries) so the probabilities come
+// out with one query per lane, and feeds them back as the A operand of P V
+// with a permuted contraction order (see ea_common.h).  K and V blocks are
+// copied into double-buffered LDS tiles by global_load_lds (the next listed
+// block in flight while the current one is consumed); V's operand fragments
+// come out of its row-major tile through transposing LDS reads.
 #include <type_traits>
 
 #include "ea_common.h"
