@@ -36,32 +36,26 @@ constexpr int TAU_WAVES = 4;
 constexpr int TAU_NT = 64 * TAU_WAVES;
 constexpr int TAU_ROWS = 32 * TAU_WAVES;
 
-// MODE: SOLVE writes tau, the block mask and stats; FUSED_O (inference) and
-// FUSED_O2 (training) are the no-mask forward of Algorithm 2: once tau is
-// known, the same workgroup streams K and V once more and writes O (and
-// O2), with no mask or tables.
-constexpr int SOLVE = 0, FUSED_O = 1, FUSED_O2 = 2;
+// MODE: FUSED_O (inference) and FUSED_O2 (training) are the no-mask forward
+// of Algorithm 2: once tau is known, the same workgroup streams K and V once
+// more and writes O (and O2), with no mask or tables.
+constexpr int FUSED_O = 1, FUSED_O2 = 2;
 
 template <typename E, int D, int GK, int MODE>
-__global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kernel(TauArgs a) {
+__global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
   using TL = PadTile<E, D>;
   using TV = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
   constexpr int NTD = D / 32;
   constexpr int PS = perm_steps<E>();
-  constexpr bool FUSED = MODE != SOLVE, TRAIN = MODE == FUSED_O2;
-  constexpr int BW = MAX_KEY_BLOCKS / 32;  // mask words per wave
+  constexpr bool TRAIN = MODE == FUSED_O2;
   __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
-  __shared__ __attribute__((aligned(16))) E vbuf[FUSED ? 2 : 1][FUSED ? TV::ELEMS : 8];
-  // bit kb of word kb / 32: key block kb holds a positive probability for
-  // one of the wave's 32 rows
-  __shared__ uint32_t bits[TAU_WAVES * BW];
+  __shared__ __attribute__((aligned(16))) E vbuf[2][TV::ELEMS];
 
   const int lane = lane_id(), w = wave_id();
   const int n = a.n, T = a.T;
   const int nqt = (n + TAU_ROWS - 1) / TAU_ROWS;
-  const int TW = (T + 31) / 32;
   const float c = a.c, g = a.gamma;
   // The Newton step from any tau is a lower bound of the root when f is
   // convex, i.e. gamma >= 1 (alpha <= 2).
@@ -94,8 +88,6 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
     typename M::frag qf[KS];
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) qf[kk] = load_row_frag_global<E, D>(Q, i, n, kk);
-
-    for (int x = threadIdx.x; x < TAU_WAVES * TW; x += TAU_NT) bits[(x / TW) * BW + (x % TW)] = 0;
 
     // Streams every key block the tile needs, double-buffered: block kb + 1
     // is copied into LDS while `body(kb, tile)` works on block kb.
@@ -226,7 +218,6 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
       }
     }
 
-    int passes = 1;      // K passes (streamed), the max pass included
     bool cached = false; // evaluations run on the candidate cache
     int attempts = 0;    // cache fills tried
     int cc = 0;          // candidates this thread found in the last fill
@@ -282,7 +273,7 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
           }
         }
       };
-      // Adds one sub-tile; returns whether it holds a positive probability.
+      // Adds one sub-tile to the sums.
       auto eval_tile = [&](const f32x16& s) {
         if constexpr (GK == 1 || GK == 2) {
           int cnt = 0;
@@ -301,14 +292,11 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
             cnt += in_support(za) + in_support(zb);
           }
           mc += cnt;
-          return cnt > 0;
         } else {
-          // tile sums start from 0, so t0 > 0 exactly when some term is > 0
-          float t0 = 0.f;
+          float t0 = 0.f;  // summed per tile, then added to the row sum
 #pragma unroll
           for (int r = 0; r < 16; ++r) add_z(relu_z(c, s[r], tau), t0, m1, m2, mc);
           m0 += t0;
-          return t0 > 0.f;
         }
       };
       // Appends the entries x > lo of a sub-tile to this thread's cache list.
@@ -355,30 +343,26 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
           if (k0) fill_tile(s0, kb);
           if (k1) fill_tile(s1, kb);
         });
-        ++passes;
         fill_done();
       }
       if (!cached) {
-        // streamed evaluation; the mask bits of every block are rewritten
+        // streamed evaluation
         const bool fill = cache && it == 0;
         if (fill) {
           ++attempts;
           cc = 0;
           if (threadIdx.x == 0) fill_full = 0;  // read after the first block's barrier
         }
-        uint32_t word = 0;  // mask bits of the current 32-block group (wave-uniform)
         stream([&](int kb, const E* kt) {
           const int j0 = kb * BLK;
           const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
-          bool any = false;
           // once a list of this fill has overflowed, no thread stores more
           const bool fill_now = fill && !fill_full;
           if (k0 == 1 && k1 == 1) {  // every key valid: one straight-line block
             f32x16 s0, s1;
             scores(kt, s0, s1);
-            const bool a0 = eval_tile(s0);
-            const bool a1 = eval_tile(s1);
-            any = a0 || a1;
+            eval_tile(s0);
+            eval_tile(s1);
             if (fill_now) {
               fill_tile(s0, kb);
               fill_tile(s1, kb);
@@ -388,21 +372,15 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
             scores(kt, s0, s1);
             if (k0 == 2) mask_tile(s0, j0);
             if (k1 == 2) mask_tile(s1, j0 + 32);
-            if (k0) any |= eval_tile(s0);
-            if (k1) any |= eval_tile(s1);
+            if (k0) eval_tile(s0);
+            if (k1) eval_tile(s1);
             if (fill_now) {
               if (k0) fill_tile(s0, kb);
               if (k1) fill_tile(s1, kb);
             }
           }
           if (fill_now && cc > a.cap) fill_full = 1;
-          if (__ballot(any) != 0ull) word |= 1u << (kb & 31);
-          if ((kb & 31) == 31 || kb == nkb - 1) {
-            if (lane == 0) bits[w * BW + (kb >> 5)] = word;
-            word = 0;
-          }
         });
-        ++passes;
         // support sizes at this tau, a guide to the size of the candidate lists
         small_support = !__syncthreads_or(mc > a.cap / 2);
         if (fill) {
@@ -472,7 +450,7 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
 
     if (row_ok && lane < 32) a.tau[(size_t)bh * n + i] = tau;
 
-    if constexpr (FUSED) {
+    {
       // ---- Algorithm 2 at the returned tau: O = sum_j P_ij V_j, and in
       // training O2 = sum_j u_ij V_j / sum_j u_ij (sum u is the solver's last
       // S1 sum), over every valid key block.
@@ -548,29 +526,6 @@ __global__ __launch_bounds__(TAU_NT, MODE == SOLVE ? 4 : 2) void tau_solve_kerne
             if constexpr (TRAIN) O2[off] = us > 0.f ? o2[nt][r] / us : 0.f;
           }
         }
-      }
-      return;
-    }
-
-    if (cached) {
-      // mask bits at the returned tau from the cached entries
-      for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
-      __syncthreads();
-      scan([&](const CandEntry& ce) {
-        if (in_support(relu_z(c, ce.s, tau))) atomicOr(&bits[w * BW + (ce.kb >> 5)], 1u << (ce.kb & 31));
-      });
-    }
-
-    __syncthreads();
-    constexpr int QBLOCKS = TAU_WAVES / 2;  // 64-row mask rows per workgroup
-    for (int x = threadIdx.x; x < QBLOCKS * T; x += TAU_NT) {
-      const int half = x / T, kb = x % T;
-      const int qb = QBLOCKS * qt + half;
-      if (qb < T) {
-        const uint32_t both = bits[(2 * half) * BW + (kb >> 5)] | bits[(2 * half + 1) * BW + (kb >> 5)];
-        const uint8_t b = (both >> (kb & 31)) & 1u;
-        a.mask[((size_t)bh * T + qb) * T + kb] = b;
-        if (a.stats && kb == 0) a.stats[(size_t)bh * T + qb] = passes;
       }
     }
   }
