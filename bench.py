@@ -120,7 +120,7 @@ def write_traffic(fetch_csv, write_csv, calib_mib, command, head_dim=128):
         w_b = sum(wk) / len(wk) * 1024.0 * w_scale if wk else 0.0
         with open(traffic_path(kernel), "w") as fh:
             fh.write("# HBM traffic of `%s` (rocprofv3 FETCH_SIZE / WRITE_SIZE)\n\n" % frag)
-            fh.write("Commands (repository root on the GPU box; `cd /tmp && export TMPDIR=/tmp` "
+            fh.write("Commands (repository root on an MI355X; `cd /tmp && export TMPDIR=/tmp` "
                      "first, one counter per run):\n\n```\n%s\n```\n\n" % command)
             fh.write("Scaling: the plain device copy of %d MiB read %.0f KiB (FETCH_SIZE) and "
                      "wrote %.0f KiB (WRITE_SIZE); each counter is multiplied by the ratio of "
@@ -468,16 +468,16 @@ def main():
     args = parse()
     if args.traffic_from:
         mib = args.calib_copy_mib or 1024
-        write_traffic(args.traffic_from[0], args.traffic_from[1], mib,
-                      "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run "
-                      "-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-configs --no-cpu-baseline "
-                      "--no-rows --calib-copy-mib %d\n"
-                      "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run "
-                      "-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-configs --no-cpu-baseline "
-                      "--no-rows --calib-copy-mib %d\n"
-                      "python bench.py --traffic-from gpurun_out/pmc_fetch/run_counter_collection.csv "
-                      "gpurun_out/pmc_write/run_counter_collection.csv --calib-copy-mib %d"
-                      % (mib, mib, mib), head_dim=args.head_dim)
+        fetch_csv, write_csv = args.traffic_from
+        # the counter runs that wrote the two files, as they were run
+        run = ("-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-configs "
+               "--no-cpu-baseline --no-rows --calib-copy-mib %d" % mib)
+        write_traffic(fetch_csv, write_csv, mib,
+                      "rocprofv3 --pmc FETCH_SIZE --output-format csv -d %s -o run %s\n"
+                      "rocprofv3 --pmc WRITE_SIZE --output-format csv -d %s -o run %s\n"
+                      "python bench.py --traffic-from %s %s --calib-copy-mib %d"
+                      % (os.path.dirname(fetch_csv), run, os.path.dirname(write_csv), run,
+                         fetch_csv, write_csv, mib), head_dim=args.head_dim)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the alpha-entmax path here is a single-GPU "
