@@ -544,6 +544,9 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
 constexpr int SV_WAVES = SOLVE_THREADS / 64;
 constexpr int SV_NT = SOLVE_THREADS;
 constexpr int SV_ROWS = SOLVE_ROWS;
+// threads (of SV_NT) with a score above the running bound in one key block
+// at or below which the solver's first stream ends early
+constexpr int WARM_STOP = SV_NT / 4;
 static_assert(SV_ROWS == 64 * SV_WAVES, "one 64-row query block per wave");
 
 // fp32 operands at d = 128 (128 registers of query fragments) run one wave
@@ -822,24 +825,61 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   float sb[2] = {-INFINITY, -INFINITY};  // collection thresholds
   __shared__ int fill_dead;              // a list overflowed: stop collecting
   if (threadIdx.x == 0) fill_dead = 0;   // read after the first block's barrier
-  // With a cache slot, a first stream over the first half of the key
-  // blocks finds their sub-tile maxima, so that the collection below starts
-  // from a bound close to its final value instead of collecting (and later
-  // dropping) most scores of its first blocks.  Those blocks' maxima are
-  // then not inserted again (the bound needs distinct keys).  (Measured at
-  // n = 8192: an eighth 0.92 ms, a quarter 0.84, a half 0.81, all 0.81.)
-  const int W = cache ? max(1, nkb / 2) : 0;
-  if (W > 0) {
-    stream_n(W, [&](int kb, const E* kt) {
+  // With a cache slot, a first stream over the leading key blocks finds
+  // their sub-tile maxima, so that the collection below starts from a bound
+  // close to its final value instead of collecting (and later dropping) most
+  // scores of its first blocks.  Those blocks' maxima are then not inserted
+  // again (the bound needs distinct keys).  The stream covers an eighth or
+  // half of the key blocks.  After the eighth it counts the threads holding
+  // a score of the last block above the bound of the maxima so far, and
+  // stops there if at most WARM_STOP of them do: for rows with few large
+  // scores the collection is cheap and a longer stream only adds MFMA work,
+  // for rows with many it saves list stores.  (Measured at n = 8192 with a
+  // fixed length: an eighth, a quarter and a half of the blocks cost 0.77 /
+  // 0.75 / 0.73 ms at c = 1, while at c = 16 and at n = 65536 causal the
+  // eighth was the fastest.  The count after an eighth is 189 of 256
+  // threads at c = 1, 95 at c = 2, 49 at c = 4 and 23 at c = 16.)
+  int W = 0;
+  if (cache) {
+    const int w_lo = max(1, nkb / 8), w_hi = max(1, nkb / 2);
+    dma.issue(kbuf[0], K, 0, n);
+    for (int kb = 0;; ++kb) {
+      dma_wait();
+      __syncthreads();
+      if (kb + 1 < w_hi) dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
       f32x16 s[2][2];
       int k[2][2];
-      if (!block(kb, kt, s, k)) return;
+      const bool valid = block(kb, kbuf[kb & 1], s, k);
+      if (valid) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int gq = 0; gq < 2; ++gq)
-          if (k[h][gq]) tile_max(s[h][gq], gq);
-    });
+          for (int gq = 0; gq < 2; ++gq)
+            if (k[h][gq]) tile_max(s[h][gq], gq);
+      }
+      W = kb + 1;
+      if (W >= w_hi) break;
+      if (W == w_lo) {
+        int above = 0;
+#pragma unroll
+        for (int gq = 0; gq < 2; ++gq) {
+          float u[8];
+          row_top8(gq, u);
+          const float b = row_ok[gq] ? score_bound(u, true) : INFINITY;
+          if (valid) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+              if (k[h][gq]) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) above += s[h][gq][r] > b ? 1 : 0;
+              }
+          }
+        }
+        if (__syncthreads_count(above > 0) <= WARM_STOP) break;
+      }
+    }
+    dma_wait();  // the copy of block W may still be in flight
+    __syncthreads();
 #pragma unroll
     for (int gq = 0; gq < 2; ++gq) {
       float u[8];
