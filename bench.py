@@ -14,7 +14,7 @@ temperature c; `executed_tflops` counts the MFMA work the method actually
 performs (solver passes over every valid block, 10 block products per listed
 block).  `roofline` is for the kernel with the largest share of the step,
 timed with HIP events over the timed region; `cpu_baseline` is the fp64
-oracle on a bounded sample (one head), on this host's cores.
+oracle on a bounded sample (four heads by default), on this host's cores.
 """
 from __future__ import annotations
 
