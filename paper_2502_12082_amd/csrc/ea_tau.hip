@@ -932,18 +932,30 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         }
       }
     }
-    // only sub-tiles whose maximum passes in some lane are searched
+    // Only sub-tiles whose maximum passes in some lane are searched, and in
+    // them only the groups of four scores whose maximum passes in some lane
+    // (most searched sub-tiles hold one entry in one lane: the per-score
+    // tests of the other groups would cost the whole wave).  The entries keep
+    // the stream's order.  (Measured against one test per score: the solver
+    // takes 8-10% less at c = 16 and at n = 65536 causal, d = 64, and 3% more
+    // at c = 1, where most groups of a searched sub-tile pass.)
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int gq = 0; gq < 2; ++gq)
         if (__ballot(tm[h][gq] > sb[gq]) != 0ull) {
+          const f32x16& t = s[h][gq];
           uint32_t off = entry_idx(cc[gq], gq);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            if (s[h][gq][r] > sb[gq]) {
-              put(off, s[h][gq][r], kb);
-              off += ENTRY_STEP;
+          for (int r0 = 0; r0 < 16; r0 += 4) {
+            const float m4 = fmaxf(fmaxf(t[r0], t[r0 + 1]), fmaxf(t[r0 + 2], t[r0 + 3]));
+            if (__ballot(m4 > sb[gq]) == 0ull) continue;
+#pragma unroll
+            for (int r = r0; r < r0 + 4; ++r) {
+              if (t[r] > sb[gq]) {
+                put(off, t[r], kb);
+                off += ENTRY_STEP;
+              }
             }
           }
           cc[gq] = (int)((off - entry_idx(0, gq)) / ENTRY_STEP);
