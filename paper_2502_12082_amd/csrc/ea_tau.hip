@@ -774,6 +774,11 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     return (uint32_t)e * ENTRY_STEP + (uint32_t)(gq * SV_NT + (int)threadIdx.x);
   };
   auto put = [&](uint32_t idx, float sv, int kbv) { cache[idx] = CandEntry{sv, kbv}; };
+  // the same store at a 32-bit byte offset from the slot base (a wave-uniform
+  // base plus a per-lane offset needs no 64-bit address arithmetic)
+  auto put_at = [&](uint32_t byte_off, float sv, int kbv) {
+    *reinterpret_cast<CandEntry*>(reinterpret_cast<char*>(cache) + byte_off) = CandEntry{sv, kbv};
+  };
   auto wave_max = [&](int v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o));
@@ -945,7 +950,8 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       for (int gq = 0; gq < 2; ++gq)
         if (__ballot(tm[h][gq] > sb[gq]) != 0ull) {
           const f32x16& t = s[h][gq];
-          uint32_t off = entry_idx(cc[gq], gq);
+          constexpr uint32_t STEP_BYTES = ENTRY_STEP * sizeof(CandEntry);
+          uint32_t off = entry_idx(cc[gq], gq) * (uint32_t)sizeof(CandEntry);
 #pragma unroll
           for (int r0 = 0; r0 < 16; r0 += 4) {
             const float m4 = fmaxf(fmaxf(t[r0], t[r0 + 1]), fmaxf(t[r0 + 2], t[r0 + 3]));
@@ -953,12 +959,12 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 #pragma unroll
             for (int r = r0; r < r0 + 4; ++r) {
               if (t[r] > sb[gq]) {
-                put(off, t[r], kb);
-                off += ENTRY_STEP;
+                put_at(off, t[r], kb);
+                off += STEP_BYTES;
               }
             }
           }
-          cc[gq] = (int)((off - entry_idx(0, gq)) / ENTRY_STEP);
+          cc[gq] = (int)((off / (uint32_t)sizeof(CandEntry) - entry_idx(0, gq)) / ENTRY_STEP);
         }
   });
 
