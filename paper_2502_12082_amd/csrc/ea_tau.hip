@@ -11,18 +11,22 @@
 // the row maximum; that pass also raises the lower end with the largest
 // scores' own bound (see pass 0) and, given a workspace, collects each row's
 // scores above it, on which every later evaluation can run without K.  The
-// block mask of Eq. 8 is recorded during every evaluation (or rebuilt from
-// the collected scores) at the returned tau, so the mask describes exactly
-// the probabilities that the forward and backward kernels recompute from
-// that tau.
+// masked path's block mask of Eq. 8 is recorded during every streamed
+// evaluation (or rebuilt from the collected scores) at the returned tau, so
+// the mask describes exactly the probabilities that the forward and backward
+// kernels recompute from that tau.
 //
-// Layout on gfx950: one workgroup = 4 waves = 128 query rows (two mask
-// rows); each wave keeps its 32 query rows as MFMA B operands in registers
-// and computes S^T tiles (keys x queries), so every lane owns one query and
-// the per-row sums stay in-lane until the end of a pass.  K tiles of 64 keys
-// are copied into a double-buffered LDS tile by global_load_lds, the next
-// one in flight while the current one is consumed.  A workgroup stops as
-// soon as every row it owns has |f(tau)| <= tol, or after max_iter updates.
+// Two kernels.  solve_kernel is the masked path's solver (tau, the block
+// mask and stats; its layout is described where it is defined).
+// tau_solve_kernel is the no-mask forward: the same solver followed, in the
+// same workgroup, by the O (and O2) pass of Algorithm 2.  Its layout on
+// gfx950: one workgroup = 4 waves = 128 query rows; each wave keeps its 32
+// query rows as MFMA B operands in registers and computes S^T tiles (keys x
+// queries), so every lane owns one query and the per-row sums stay in-lane
+// until the end of a pass.  In both, K tiles of 64 keys are copied into a
+// double-buffered LDS tile by global_load_lds, the next one in flight while
+// the current one is consumed, and a workgroup stops as soon as every row it
+// owns has |f(tau)| <= tol, or after max_iter updates.
 #include <type_traits>
 
 #include "ea_common.h"
