@@ -550,7 +550,7 @@ constexpr int SV_NT = SOLVE_THREADS;
 constexpr int SV_ROWS = SOLVE_ROWS;
 // threads (of SV_NT) with a score above the running bound in one key block
 // at or below which the solver's first stream ends early
-constexpr int WARM_STOP = SV_NT / 4;
+constexpr int WARM_STOP = SV_NT / 2;
 static_assert(SV_ROWS == 64 * SV_WAVES, "one 64-row query block per wave");
 
 // fp32 operands at d = 128 (128 registers of query fragments) run one wave
