@@ -210,6 +210,82 @@ def _stream_handle(device):
     return torch.cuda.current_stream(device).cuda_stream
 
 
+# ------------------------------------------------------ argument checks
+#
+# The C ABI takes bare device pointers and no sizes for the residual buffers,
+# so a tensor of the wrong shape, dtype or device would make the kernels read
+# or write past its end.  Every tensor is checked here before any call.
+
+def _need(t, name, shape, dtype, device=None):
+    """Raises ValueError unless t is a contiguous tensor of this shape and
+    dtype (and, given device, on that device).  Whether that device is a GPU
+    is checked once per call by _on_gpu, after every tensor's shape."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError("%s must be a torch tensor" % name)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    if t.dtype != dtype:
+        raise ValueError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+
+
+def _on_gpu(device):
+    if device is None or device.type != "cuda":
+        raise ValueError("tensors must be on a GPU device, not %s" % device)
+
+
+def _torch_dtype(shape: Shape):
+    return torch.bfloat16 if shape.dtype == EA_BF16 else torch.float32
+
+
+def _check_qkv(names_tensors, shape: Shape):
+    """q, k, v (and dO) against one shape: [B, H, n, d] in the shape's dtype,
+    all on the device of the first."""
+    dims = (shape.batch, shape.heads, shape.seqlen, shape.head_dim)
+    dev = names_tensors[0][1].device if isinstance(names_tensors[0][1], torch.Tensor) else None
+    for name, t in names_tensors:
+        _need(t, name, dims, _torch_dtype(shape), dev)
+    return dev
+
+
+def _same_shape(a: Shape, b: Shape) -> bool:
+    return all(getattr(a, f) == getattr(b, f) for f, _ in Shape._fields_)
+
+
+def _check_residuals(res, shape: Shape, device, need_o2: bool):
+    if not isinstance(res, Residuals):
+        raise ValueError("res must be the Residuals of a forward call")
+    if not _same_shape(res.shape, shape):
+        raise ValueError("res was sized for a different shape or dtype")
+    BH, n, d = shape.batch * shape.heads, shape.seqlen, shape.head_dim
+    T = (n + 63) // 64
+    _need(res.tau, "res.tau", (BH, n), torch.float32, device)
+    if need_o2:
+        if res.o2 is None:
+            raise ValueError("res has no o2 (forward ran with need_bwd=False)")
+        _need(res.o2, "res.o2", (BH, n, d), torch.float32, device)
+    _need(res.block_mask, "res.block_mask", (BH, T, T), torch.uint8, device)
+    _need(res.q_count, "res.q_count", (BH, T), torch.int32, device)
+    _need(res.q_index, "res.q_index", (BH, T, T), torch.int32, device)
+    _need(res.k_count, "res.k_count", (BH, T), torch.int32, device)
+    _need(res.k_index, "res.k_index", (BH, T, T), torch.int32, device)
+    if res.stats is not None:
+        _need(res.stats, "res.stats", (res.sizes.stats // 4,), torch.int32, device)
+
+
+def _check_bytes(ws, name, need_bytes, device):
+    if not isinstance(ws, torch.Tensor) or not ws.is_contiguous():
+        raise ValueError("%s must be a contiguous tensor" % name)
+    if ws.numel() * ws.element_size() < need_bytes:
+        raise ValueError("%s holds %d bytes, needs %d" % (
+            name, ws.numel() * ws.element_size(), need_bytes))
+    if ws.device != device:
+        raise ValueError("%s must be on %s" % (name, device))
+
+
 def forward_workspace(res: Residuals, device):
     """A device buffer of sizes.ws_fwd bytes for the solver's candidate cache."""
     return torch.empty(max(res.sizes.ws_fwd, 16), dtype=torch.uint8, device=device)
@@ -221,15 +297,20 @@ def forward(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_ite
 
     workspace: a uint8 device tensor for the solver's candidate cache (None
     allocates sizes.ws_fwd bytes; False runs the solver without the cache)."""
-    for t in (q, k, v):
-        if not t.is_cuda or not t.is_contiguous() or t.shape != q.shape or t.dtype != q.dtype:
-            raise ValueError("q, k, v must be contiguous device tensors of one shape and dtype")
     shape = make_shape(q)
+    dev = _check_qkv([("q", q), ("k", k), ("v", v)], shape)
     params = make_params(alpha, scale, causal, need_bwd, max_iter, tol, head_dim=q.shape[-1])
     if res is None:
         res = Residuals(shape, params, q.device)
+    else:
+        _check_residuals(res, shape, dev, bool(need_bwd))
     if out is None:
         out = torch.empty_like(q)
+    else:
+        _need(out, "out", q.shape, q.dtype, dev)
+    if workspace is not None and workspace is not False:
+        _check_bytes(workspace, "workspace", 0, dev)
+    _on_gpu(dev)
     rp = res.ptrs()
     if workspace is None:
         workspace = forward_workspace(res, q.device)
@@ -245,13 +326,20 @@ def forward(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_ite
 def backward(q, k, v, dout, res: Residuals, dq=None, dk=None, dv=None, workspace=None):
     """(dQ, dK, dV) in fp32 for the loss sum(dO * O) of the forward that filled res."""
     shape = make_shape(q)
-    if dout.shape != q.shape or dout.dtype != q.dtype or not dout.is_contiguous():
-        raise ValueError("dout must match q")
+    dev = _check_qkv([("q", q), ("k", k), ("v", v), ("dout", dout)], shape)
+    _check_residuals(res, shape, dev, True)
+    if not res.params.need_bwd:
+        raise ValueError("res comes from a forward with need_bwd=False")
     mk = lambda t: t if t is not None else torch.empty(q.shape, dtype=torch.float32, device=q.device)
     dq, dk, dv = mk(dq), mk(dk), mk(dv)
+    for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _need(t, name, q.shape, torch.float32, dev)
     if workspace is None:
         workspace = torch.empty(max(res.sizes.ws_bwd, 16) // 4 + 4, dtype=torch.float32,
                                 device=q.device)
+    else:
+        _check_bytes(workspace, "workspace", res.sizes.ws_bwd, dev)
+    _on_gpu(dev)
     rp = res.ptrs()
     _check(entmax_attn_bwd(shape, res.params, q.data_ptr(), k.data_ptr(), v.data_ptr(),
                            dout.data_ptr(), rp, dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
@@ -297,10 +385,14 @@ def rows_forward(s, alpha=1.5, scale=1.0, max_iter=None, tol=None):
 
 def rows_backward(s, tau, dp, alpha=1.5, scale=1.0):
     """Gradient of sum(dp * p) with respect to s, for (p, tau) = rows_forward(s)."""
+    if not isinstance(s, torch.Tensor) or s.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("s must be a bf16 or fp32 tensor")
+    _need(s, "s", s.shape, s.dtype)
     n = s.shape[-1]
     rows = s.numel() // n
-    if dp.shape != s.shape or dp.dtype != torch.float32 or not dp.is_contiguous():
-        raise ValueError("dp must be a contiguous fp32 tensor shaped like s")
+    _need(dp, "dp", s.shape, torch.float32, s.device)
+    _need(tau, "tau", s.shape[:-1], torch.float32, s.device)
+    _on_gpu(s.device)
     ds = torch.empty(s.shape, dtype=torch.float32, device=s.device)
     params = _row_params(alpha, scale, None, None)
     _check(entmax_rows_bwd(rows, n, EA_BF16 if s.dtype == torch.bfloat16 else EA_F32, params,
@@ -315,6 +407,8 @@ def forward_dense(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, m
                   tol=None, workspace=None):
     """(O, tau, O2 or None) without block mask or tables (Algorithm 2 as written)."""
     shape = make_shape(q)
+    dev = _check_qkv([("q", q), ("k", k), ("v", v)], shape)
+    _on_gpu(dev)
     params = make_params(alpha, scale, causal, need_bwd, max_iter, tol, head_dim=q.shape[-1])
     B, H, n, d = q.shape
     o = torch.empty_like(q)
@@ -323,6 +417,9 @@ def forward_dense(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, m
     z = entmax_attn_sizes(shape, params)
     if workspace is None:
         workspace = torch.empty(max(z.ws_fwd, 16), dtype=torch.uint8, device=q.device)
+    elif workspace is not False:
+        _check_bytes(workspace, "workspace", 0, dev)
+    _on_gpu(dev)
     ws_ptr, ws_bytes = (None, 0) if workspace is False else (workspace.data_ptr(),
                                                             workspace.numel() * workspace.element_size())
     _check(_lib.entmax_attn_fwd_dense(ctypes.byref(shape), ctypes.byref(params), q.data_ptr(),
@@ -335,6 +432,11 @@ def forward_dense(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, m
 def backward_dense(q, k, v, dout, tau, o2, alpha=1.5, scale=None, causal=False):
     """(dQ, dK, dV) in fp32 for the no-mask forward that produced tau and o2."""
     shape = make_shape(q)
+    dev = _check_qkv([("q", q), ("k", k), ("v", v), ("dout", dout)], shape)
+    B, H, n, d = q.shape
+    _need(tau, "tau", (B * H, n), torch.float32, dev)
+    _need(o2, "o2", q.shape, torch.float32, dev)
+    _on_gpu(dev)
     params = make_params(alpha, scale, causal, True, None, None, head_dim=q.shape[-1])
     z = entmax_attn_sizes(shape, params)
     mk = lambda: torch.empty(q.shape, dtype=torch.float32, device=q.device)

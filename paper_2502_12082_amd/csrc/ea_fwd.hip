@@ -13,6 +13,13 @@
 // O2_i = U V / sum U (the O^(2) of App. A.2).  O is not renormalised: the
 // row sums are 1 + f(tau) of the returned tau (Algorithm 1 output).
 //
+// Precision: S is a bf16 x bf16 product accumulated in fp32; P and U enter
+// their products with V as two-term bf16 splits (hi + lo, ~16 significant
+// bits), so the only rounding of O beyond fp32 accumulation is its final
+// rounding to the input dtype.  With P rounded once to bf16, a row whose
+// probability sits on one key (p ~ 1, |v| ~ 5) would carry 2^-9 |v| ~ 0.01
+// of operand error on top of the 0.0156 that rounding O ~ 5 to bf16 costs.
+//
 // gfx950 layout: one workgroup = 4 waves = one 64-row query block; each wave
 // holds 32 query rows as MFMA B operands and takes one 32-key half of every
 // listed key block, computes S^T (keys x queries) so the probabilities come
@@ -159,13 +166,14 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
     }
 #pragma unroll
     for (int t = 0; t < PS; ++t) {
-      const typename M::frag pa = M::pack(p, t);
-      typename M::frag uh, ul;
+      typename M::frag ph, pl, uh, ul;
+      M::pack_split(p, t, ph, pl);
       if constexpr (TRAIN) M::pack_split(u, t, uh, ul);
 #pragma unroll
       for (int nt = 0; nt < NTD; ++nt) {
         const typename M::frag vb = lds_perm_frag<E, D>(vt, 32 * nt, 32 * kh, t);
-        o[nt] = M::mma(pa, vb, o[nt]);
+        o[nt] = M::mma(ph, vb, o[nt]);
+        if constexpr (!M::exact_operands) o[nt] = M::mma(pl, vb, o[nt]);
         if constexpr (TRAIN) {
           o2[nt] = M::mma(uh, vb, o2[nt]);
           if constexpr (!M::exact_operands) o2[nt] = M::mma(ul, vb, o2[nt]);

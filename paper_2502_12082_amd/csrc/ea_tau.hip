@@ -479,13 +479,14 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
         }
 #pragma unroll
         for (int t = 0; t < PS; ++t) {
-          const typename M::frag pa = M::pack(p, t);
-          typename M::frag uh, ul;
+          typename M::frag ph, pl, uh, ul;
+          M::pack_split(p, t, ph, pl);
           if constexpr (TRAIN) M::pack_split(u, t, uh, ul);
 #pragma unroll
           for (int nt = 0; nt < NTD; ++nt) {
             const typename M::frag vb = lds_perm_frag<E, D>(vt, 32 * nt, 32 * sub, t);
-            o[nt] = M::mma(pa, vb, o[nt]);
+            o[nt] = M::mma(ph, vb, o[nt]);
+            if constexpr (!M::exact_operands) o[nt] = M::mma(pl, vb, o[nt]);
             if constexpr (TRAIN) {
               o2[nt] = M::mma(uh, vb, o2[nt]);
               if constexpr (!M::exact_operands) o2[nt] = M::mma(ul, vb, o2[nt]);

@@ -13,6 +13,16 @@ BF16_TOL = 2e-2    # max-abs for O, O2, dQ, dK, dV with bf16 inputs
 F32_TOL = 1e-4     # max-abs with fp32 inputs
 TAU_REL = 1e-3     # |dtau| <= TAU_REL * max(1, |tau|)
 MASK_BAND = 1e-4   # blocks with |margin| <= MASK_BAND * max(1, |tau|) may legitimately flip
+# Blocks inside that band are few: the band is ~1e-4 |tau| wide while block
+# margins spread over O(1), so about 1e-3 of the blocks (15 of the 16384 of
+# one n = 8192 head at c = 4).  More than MASK_BAND_FRAC of the checked
+# blocks (plus a few) means the band is too wide to be a meaningful check.
+MASK_BAND_FRAC = 2e-3
+# The GPU's own mask against its own tau (Sec. 3.2.1: a block may be skipped
+# only if all its probabilities are zero): fp64 margins at the GPU's tau must
+# be <= 0 on every skipped block and > 0 on every kept one, up to the fp32
+# rounding of the GPU's scores, SELF_BAND * max(1, |tau|).
+SELF_BAND = 2e-5
 
 
 def log(msg: str):
@@ -30,8 +40,10 @@ def to_device(t: synth.Tensor):
 
 
 def run_gpu(inp: dict, alpha: float, scale: float, causal: bool, bwd: bool, max_iter=None,
-            tol=None, device_inputs=None):
-    """All outputs of the HIP path as numpy arrays (float64 for float data)."""
+            tol=None, device_inputs=None, heads=None):
+    """All outputs of the HIP path as numpy arrays (float64 for float data).
+    heads: copy the [n, d] outputs (O, O2, dQ, dK, dV) of these heads only,
+    as a dict {bh: array}; None copies every head."""
     import torch
     import paper_2502_12082_amd as ea
     q, k, v = device_inputs or (to_device(inp["q"]), to_device(inp["k"]), to_device(inp["v"]))
@@ -49,13 +61,18 @@ def run_gpu(inp: dict, alpha: float, scale: float, causal: bool, bwd: bool, max_
     if bwd:
         out["o2"] = res.o2
     host = {}
+    BH = B * H
+    big = ("o", "o2", "dq", "dk", "dv")
     for key, val in out.items():
+        if key in big:
+            val = val.reshape(BH, n, d)
+            if heads is not None:
+                host[key] = {bh: val[bh].cpu().numpy().astype(np.float64) for bh in heads}
+                continue
         a = val.cpu().numpy()
         host[key] = a.astype(np.float64) if a.dtype.kind == "f" else a
-    BH = B * H
-    for key in ("o", "o2", "dq", "dk", "dv"):
-        if key in host:
-            host[key] = host[key].reshape(BH, n, d)
+    host["inputs"] = inp
+    host["params"] = (alpha, scale, causal)
     return host
 
 
@@ -133,6 +150,7 @@ def check_head(gpu: dict, ref: dict, bh: int, dtype: str, label: str, rows=None,
     if "margin" in ref:
         errs.update(check_mask(gpu["mask"][bh], ref["margin"], ref["tau"], n,
                                ref.get("block_rows"), label))
+        errs.update(check_mask_self(gpu, bh, ref.get("block_rows"), label))
     return errs
 
 
@@ -140,7 +158,7 @@ def check_mask(mask, margin, tau_ref, n, block_rows, label):
     """Bit-exact outside the guard band |margin| <= MASK_BAND * max(1, |tau|)."""
     T = mask.shape[0]
     rows = range(T) if block_rows is None else block_rows
-    flips = band = 0
+    flips = band = band_flips = checked = 0
     for I in rows:
         t = tau_ref[I * 64:min(n, I * 64 + 64)]
         g = MASK_BAND * max(1.0, float(np.nanmax(np.abs(t))))
@@ -150,8 +168,47 @@ def check_mask(mask, margin, tau_ref, n, block_rows, label):
         band += int(inband.sum())
         bad = (mask[I] != ref) & ~inband
         flips += int(bad.sum())
+        band_flips += int(((mask[I] != ref) & inband).sum())
+        checked += int(np.isfinite(m).sum())
     assert flips == 0, (label, "mask differs outside the guard band", flips)
-    return {"mask_band_blocks": band}
+    assert band <= 4 + MASK_BAND_FRAC * checked, (label, "blocks inside the guard band", band,
+                                                  checked)
+    return {"mask_band_blocks": band, "mask_band_flips": band_flips, "mask_blocks": checked}
+
+
+def check_mask_self(gpu: dict, bh: int, block_rows, label):
+    """The GPU's mask describes exactly the probabilities at the GPU's own
+    tau: with the margins max (x_ij - tau_gpu_i) of each block, in fp64 from
+    the same input values, a skipped block has margin <= 0 and a kept block
+    margin > 0, outside a band that covers the fp32 rounding of the GPU's
+    scores (Sec. 3.2.1: only blocks whose probabilities are all zero may be
+    skipped).  Returns the number of blocks inside that band."""
+    inp = gpu["inputs"]
+    alpha, scale, causal = gpu["params"]
+    B, H, n, d = inp["q"].shape
+    b, h = divmod(bh, H)
+    tau = gpu["tau"][bh]
+    margin = oracle.head_block_margin(inp["q"].f64()[b, h], inp["k"].f64()[b, h], alpha, scale,
+                                      causal, tau, block_rows=block_rows)
+    mask = gpu["mask"][bh]
+    T = mask.shape[0]
+    rows = range(T) if block_rows is None else block_rows
+    band = 0
+    for I in rows:
+        t = tau[I * 64:min(n, I * 64 + 64)]
+        g = SELF_BAND * max(1.0, float(np.max(np.abs(t))))
+        m = margin[I]
+        if causal:  # blocks entirely above the diagonal hold no valid pair
+            m = np.where(np.arange(T) > I, -np.inf, m)
+        inband = np.abs(m) <= g
+        band += int(inband.sum())
+        skipped_but_positive = (mask[I] == 0) & (m > g)
+        kept_but_empty = (mask[I] == 1) & (m < -g)
+        assert not skipped_but_positive.any(), (label, "a skipped block has p > 0 at the GPU tau",
+                                                I, np.nonzero(skipped_but_positive)[0])
+        assert not kept_but_empty.any(), (label, "a kept block has no p > 0 at the GPU tau",
+                                          I, np.nonzero(kept_but_empty)[0])
+    return {"self_band_blocks": band}
 
 
 def check_tables(gpu: dict, causal: bool):

@@ -54,9 +54,9 @@ def test_sizes():
     assert z.q_count == z.k_count == BH * T * 4
     assert z.q_index == z.k_index == BH * T * T * 4
     assert z.stats == BH * T * 4
-    # solver cache: whole slots of 128 entries x 256 threads x 8 bytes (no
-    # slots without a device to size them for)
-    assert z.ws_fwd % (128 * 256 * 8) == 0 and z.ws_bwd == BH * n * 4
+    # solver cache: one slot per 256-row tile, each 2 lists x 192 entries x
+    # 256 threads x 8 bytes
+    assert z.ws_fwd == BH * ((n + 255) // 256) * (2 * 192 * 256 * 8) and z.ws_bwd == BH * n * 4
 
 
 @pytest.mark.parametrize("field,value,code", [
@@ -189,3 +189,75 @@ def test_dense_mode_validation():
              None) == ea.EA_ERR_WORKSPACE
     assert b(s, p, *args, None, _fake(), _fake(), _fake(), _fake(), _fake(), z.ws_bwd,
              None) == ea.EA_ERR_INVALID_ARG
+
+
+# ------------------------------------------- binding argument checks (CPU)
+#
+# The C ABI takes no sizes for the residual buffers, so the binding refuses
+# any tensor whose shape, dtype, layout or device does not match before a
+# call is made.  CPU tensors exercise every check; the last one (the device
+# is a GPU) then refuses them as well.
+
+torch = pytest.importorskip("torch")
+
+
+def _bf(*shape):
+    return torch.zeros(*shape, dtype=torch.bfloat16)
+
+
+def test_binding_refuses_mismatched_inputs():
+    q = _bf(1, 2, 64, 64)
+    with pytest.raises(ValueError, match="k has shape"):
+        ea.forward(q, _bf(1, 2, 65, 64), q)
+    with pytest.raises(ValueError, match="v has dtype"):
+        ea.forward(q, q, q.float())
+    with pytest.raises(ValueError, match="contiguous"):
+        ea.forward(q, _bf(1, 2, 64, 128)[..., ::2], q)
+    with pytest.raises(ValueError, match="GPU"):
+        ea.forward(q, q, q)
+    with pytest.raises(ValueError, match="out has shape"):
+        ea.forward(q, q, q, out=_bf(1, 2, 64, 65))
+
+
+def test_binding_refuses_mismatched_residuals():
+    q = _bf(1, 2, 64, 64)
+    shape, params = ea.make_shape(q), ea.make_params(head_dim=64)
+    res = ea.Residuals(shape, params, "cpu")
+    q2 = _bf(1, 2, 128, 64)
+    with pytest.raises(ValueError, match="different shape"):
+        ea.backward(q2, q2, q2, q2, res)
+    with pytest.raises(ValueError, match="dout has shape"):
+        ea.backward(q, q, q, q2, res)
+    with pytest.raises(ValueError, match="dq has dtype"):
+        ea.backward(q, q, q, q, res, dq=q)
+    with pytest.raises(ValueError, match="workspace holds"):
+        ea.backward(q, q, q, q, res, workspace=torch.zeros(3))
+    res.tau = torch.zeros(2, 63)
+    with pytest.raises(ValueError, match="res.tau has shape"):
+        ea.backward(q, q, q, q, res)
+    res = ea.Residuals(shape, params, "cpu")
+    res.o2 = None
+    with pytest.raises(ValueError, match="no o2"):
+        ea.backward(q, q, q, q, res)
+    res = ea.Residuals(shape, params, "cpu")
+    res.k_index = res.k_index.to(torch.int64)
+    with pytest.raises(ValueError, match="res.k_index has dtype"):
+        ea.forward(q, q, q, res=res)
+    res = ea.Residuals(shape, params, "cpu")
+    with pytest.raises(ValueError, match="GPU"):
+        ea.backward(q, q, q, q, res)
+
+
+def test_binding_refuses_mismatched_dense_and_rows():
+    q = _bf(1, 2, 64, 64)
+    with pytest.raises(ValueError, match="tau has shape"):
+        ea.backward_dense(q, q, q, q, torch.zeros(2, 65), torch.zeros(1, 2, 64, 64))
+    with pytest.raises(ValueError, match="o2 has dtype"):
+        ea.backward_dense(q, q, q, q, torch.zeros(2, 64), q)
+    s = torch.zeros(4, 100)
+    with pytest.raises(ValueError, match="tau has shape"):
+        ea.rows_backward(s, torch.zeros(5), torch.zeros(4, 100))
+    with pytest.raises(ValueError, match="dp has dtype"):
+        ea.rows_backward(s, torch.zeros(4), torch.zeros(4, 100, dtype=torch.float64))
+    with pytest.raises(ValueError, match="GPU"):
+        ea.rows_backward(s, torch.zeros(4), torch.zeros(4, 100))

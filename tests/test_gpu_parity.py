@@ -34,7 +34,7 @@ def _full_case(B, H, n, d, dtype, alpha, causal, bwd, c, seed, heads=None, label
     scale = d ** -0.5
     log("case %s B%d H%d n%d d%d %s alpha=%g causal=%d bwd=%d c=%g" % (
         label, B, H, n, d, dtype, alpha, causal, bwd, c))
-    gpu = run_gpu(inp, alpha, scale, causal, bwd)
+    gpu = run_gpu(inp, alpha, scale, causal, bwd, heads=heads)
     check_tables(gpu, causal)
     errs = []
     for bh in (heads if heads is not None else range(B * H)):
@@ -85,7 +85,7 @@ def _sampled_case(B, H, n, d, alpha, causal, c, block_rows, ncols, heads, label,
                                  seed=synth.SEED_BASE)
     scale = d ** -0.5
     log("case %s B%d H%d n%d d%d alpha=%g causal=%d c=%g" % (label, B, H, n, d, alpha, causal, c))
-    gpu = run_gpu(inp, alpha, scale, causal, True)
+    gpu = run_gpu(inp, alpha, scale, causal, True, heads=heads)
     T = (n + 63) // 64
     rows = sorted(set(r for I in block_rows for r in range(I * 64, min(n, I * 64 + 64))))
     cols = list(range(n - ncols, n)) if ncols else None
@@ -101,23 +101,23 @@ def _sampled_case(B, H, n, d, alpha, causal, c, block_rows, ncols, heads, label,
     return gpu, inp
 
 
-# The bench workload: B1 H16 n8192 d128 bf16 non-causal, fwd+bwd, alpha 1.5.
-@pytest.mark.parametrize("alpha,c", [(1.5, 1.0), (1.5, 0.0625), (1.5, 32.0), (1.25, 1.0),
-                                     (1.25, 8.0), (2.0, 1.0), (2.0, 32.0)])
+# The sparsity sweep (B1 H16 n8192 d128 bf16 non-causal, fwd+bwd): every
+# (alpha, c) point that bench.py reports, one whole head each (every row and
+# column of tau, O, O2, dQ, dK, dV and every block of the mask).
+SWEEP_POINTS = ([(1.5, c) for c in (0.0625, 0.25, 1.0, 2.0, 4.0, 8.0, 16.0, 32.0)]
+                + [(a, c) for a in (1.25, 2.0) for c in (1.0, 2.0, 4.0, 8.0, 16.0, 32.0)])
+
+
+@pytest.mark.parametrize("alpha,c", SWEEP_POINTS)
 def test_sweep_workload(alpha, c):
-    T = 128
-    _sampled_case(1, 16, 8192, 128, alpha, False, c, block_rows=[0, 57, T - 1], ncols=0,
-                  heads=[3], label="sweep")
-
-
-def test_sweep_workload_full_head():
-    """Every row and column of one head of the bench workload (alpha 1.5, c 1)."""
-    inp = synth.attention_inputs(1, 16, 8192, 128, c=1.0, dtype="bf16", with_dout=True,
+    bh = 3
+    inp = synth.attention_inputs(1, 16, 8192, 128, c=c, dtype="bf16", with_dout=True,
                                  seed=synth.SEED_BASE)
-    gpu = run_gpu(inp, 1.5, 128 ** -0.5, False, True)
+    log("case sweep B1 H16 n8192 d128 alpha=%g c=%g (head %d)" % (alpha, c, bh))
+    gpu = run_gpu(inp, alpha, 128 ** -0.5, False, True, heads=[bh])
     check_tables(gpu, False)
-    ref = oracle_head(inp, 5, 1.5, 128 ** -0.5, False, True)
-    log("  errors %s" % check_head(gpu, ref, 5, "bf16", "sweep-full"))
+    ref = oracle_head(inp, bh, alpha, 128 ** -0.5, False, True)
+    log("  errors %s" % check_head(gpu, ref, bh, "bf16", "sweep a=%g c=%g" % (alpha, c)))
 
 
 @pytest.mark.parametrize("causal", [False, True])
@@ -135,13 +135,16 @@ def test_dkdv_sparse_key_block_pairs(causal):
     assert differ, "the chosen pairs should have different query-block lists"
 
 
-@pytest.mark.parametrize("n", [16384, 65536])
+@pytest.mark.parametrize("n", [16384, 32768, 65536])
 def test_long_context(n):
-    """B1 H8 d64 bf16 causal, c=16, fwd+bwd: first, middle and last query
-    blocks; dK/dV on the last 64 keys."""
+    """B1 H8 d64 bf16 causal, c=16, fwd+bwd (every sequence length bench.py
+    reports): first, middle and last query blocks; dK/dV on the last 64 keys
+    (which depend only on the sampled last rows under causal masking), and at
+    n = 16384 also on a key block in the middle (rows from there on)."""
     T = n // 64
+    col_blocks = [T // 2, T - 1] if n <= 16384 else None
     gpu, _ = _sampled_case(1, 8, n, 64, 1.5, True, 16.0, block_rows=[0, T // 2, T - 1],
-                           ncols=64, heads=[0, 7], label="long")
+                           ncols=64, heads=[0, 7], label="long", col_blocks=col_blocks)
     check_tables({k: gpu[k][:1] for k in ("mask", "q_count", "q_index", "k_count", "k_index")},
                  True)
 
