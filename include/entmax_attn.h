@@ -157,6 +157,26 @@ ea_status entmax_attn_bwd_stage(int stage, const ea_shape* shape, const ea_param
                                 void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * The backward without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Arguments, results and errors are those of
+ * entmax_attn_bwd; delta lives in a scratch array inside the library instead
+ * of a caller workspace: EA_NOALLOC_MAX_ROWS fp32 values (4 MiB), one copy per
+ * device, held until the process ends.  batch * heads * seqlen above
+ * EA_NOALLOC_MAX_ROWS returns EA_ERR_UNSUPPORTED before anything is launched.
+ * Nothing is allocated: the first call on a device looks up the array's
+ * address there (hipGetSymbolAddress, no allocation).  Every call on one
+ * device shares that array, so calls that overlap on one device (concurrent
+ * streams, or threads) race and must be serialised by the caller; calls on
+ * one stream are ordered.  Launches 3 kernels on `stream`.
+ */
+#define EA_NOALLOC_MAX_ROWS 1048576
+ea_status entmax_attn_bwd_noalloc(const ea_shape* shape, const ea_params* params, const void* q,
+                                  const void* k, const void* v, const void* dout,
+                                  const ea_residuals* res, float* dq, float* dk, float* dv,
+                                  void* stream);
+
+/*
  * No-mask ("memory-efficient") mode, Algorithm 2 as written (Sec. 3.2.1): the
  * forward solves tau and accumulates O (and, if need_bwd, o2) in one kernel
  * per 128-row query tile, visiting every valid key block; no block mask or

@@ -34,7 +34,9 @@ EA_BF16, EA_F32 = 0, 1
 SYMBOLS = ("entmax_attn_default_params", "entmax_attn_sizes", "entmax_attn_fwd",
            "entmax_attn_bwd", "entmax_attn_fwd_stage", "entmax_attn_bwd_stage",
            "entmax_attn_status_string", "entmax_attn_last_hip_error", "entmax_rows_fwd",
-           "entmax_rows_bwd", "entmax_attn_fwd_dense", "entmax_attn_bwd_dense")
+           "entmax_rows_bwd", "entmax_attn_fwd_dense", "entmax_attn_bwd_dense",
+           "entmax_attn_bwd_noalloc")
+NOALLOC_MAX_ROWS = 1048576  # EA_NOALLOC_MAX_ROWS of include/entmax_attn.h
 
 
 class Shape(ctypes.Structure):
@@ -92,6 +94,9 @@ _lib.entmax_rows_fwd.restype = ctypes.c_int
 _lib.entmax_rows_bwd.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int, _P(Params), _v, _v,
                                  _v, _v, _v]
 _lib.entmax_rows_bwd.restype = ctypes.c_int
+_lib.entmax_attn_bwd_noalloc.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _P(ResidualPtrs),
+                                         _v, _v, _v, _v]
+_lib.entmax_attn_bwd_noalloc.restype = ctypes.c_int
 _lib.entmax_attn_last_hip_error.argtypes = []
 _lib.entmax_attn_last_hip_error.restype = ctypes.c_char_p
 
@@ -136,6 +141,11 @@ def entmax_attn_bwd(shape, params, q, k, v, dout, res: ResidualPtrs, dq, dk, dv,
                     ws_bytes, stream):
     return _lib.entmax_attn_bwd(ctypes.byref(shape), ctypes.byref(params), q, k, v, dout,
                                 ctypes.byref(res), dq, dk, dv, workspace, ws_bytes, stream)
+
+
+def entmax_attn_bwd_noalloc(shape, params, q, k, v, dout, res: ResidualPtrs, dq, dk, dv, stream):
+    return _lib.entmax_attn_bwd_noalloc(ctypes.byref(shape), ctypes.byref(params), q, k, v, dout,
+                                        ctypes.byref(res), dq, dk, dv, stream)
 
 
 def entmax_attn_fwd_stage(stage, shape, params, q, k, v, o, res: ResidualPtrs, workspace,

@@ -4,8 +4,18 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/entmax_attn.h"
 #include "ea_internal.h"
+
+// Scratch of entmax_attn_bwd_noalloc: delta (one fp32 per row) lives here
+// instead of in a caller workspace.  Each device holds its own copy for the
+// life of the process.  In host code `scratch` only names the symbol: its
+// device address comes from hipGetSymbolAddress (scratch_for below), taken
+// once per device with that device current, and only that address is passed
+// to kernels.
+static __device__ __align__(256) float scratch[EA_NOALLOC_MAX_ROWS];
 
 namespace ea {
 
@@ -137,6 +147,36 @@ ea_status from_hip(hipError_t e) {
   return EA_ERR_HIP;
 }
 
+constexpr int MAX_DEVICES = 64;
+std::mutex scratch_mutex;
+float* scratch_ptr[MAX_DEVICES] = {};
+
+// Device address of `scratch` on the device that `stream` belongs to (the
+// current device for the null stream); null on failure with *err set.
+float* scratch_for(hipStream_t stream, hipError_t* err) {
+  int dev = 0;
+  *err = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (*err != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= MAX_DEVICES) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (scratch_ptr[dev]) return scratch_ptr[dev];
+  int cur = 0;
+  if ((*err = hipGetDevice(&cur)) != hipSuccess) return nullptr;
+  if (cur != dev && (*err = hipSetDevice(dev)) != hipSuccess) return nullptr;
+  void* p = nullptr;
+  *err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (cur != dev) {
+    const hipError_t e2 = hipSetDevice(cur);
+    if (*err == hipSuccess) *err = e2;
+  }
+  if (*err != hipSuccess) return nullptr;
+  scratch_ptr[dev] = static_cast<float*>(p);
+  return scratch_ptr[dev];
+}
+
 }  // namespace
 }  // namespace ea
 
@@ -207,16 +247,25 @@ ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const
   return from_hip(launch_fwd(fa, d.dtype, (int)d.d, params->need_bwd != 0, s));
 }
 
-ea_status prep_bwd(const ea_shape* shape, const ea_params* params, const void* q, const void* k,
-                   const void* v, const void* dout, const ea_residuals* res, const float* dq,
-                   const float* dk, const float* dv, const void* workspace, size_t ws_bytes,
-                   Dims* d) {
+// Checks of the backward's tensors and residuals (not its workspace).
+ea_status prep_bwd_args(const ea_shape* shape, const ea_params* params, const void* q,
+                        const void* k, const void* v, const void* dout, const ea_residuals* res,
+                        const float* dq, const float* dk, const float* dv, Dims* d) {
   ea_status st = check_shape(shape, params, d);
   if (st != EA_OK) return st;
   if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(dout)) return EA_ERR_INVALID_ARG;
   if (!tensor_ok(dq) || !tensor_ok(dk) || !tensor_ok(dv)) return EA_ERR_INVALID_ARG;
   if ((st = check_tables(res)) != EA_OK) return st;
   if (!tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
+  return EA_OK;
+}
+
+ea_status prep_bwd(const ea_shape* shape, const ea_params* params, const void* q, const void* k,
+                   const void* v, const void* dout, const ea_residuals* res, const float* dq,
+                   const float* dk, const float* dv, const void* workspace, size_t ws_bytes,
+                   Dims* d) {
+  ea_status st = prep_bwd_args(shape, params, q, k, v, dout, res, dq, dk, dv, d);
+  if (st != EA_OK) return st;
   if (!workspace || !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
   if (ws_bytes < bwd_ws_bytes(*d)) return EA_ERR_WORKSPACE;
   return EA_OK;
@@ -290,6 +339,25 @@ ea_status entmax_attn_bwd_stage(int stage, const ea_shape* shape, const ea_param
   if (st != EA_OK) return st;
   return run_bwd_stage(stage, d, params, q, k, v, dout, res, dq, dk, dv, workspace,
                        static_cast<hipStream_t>(stream));
+}
+
+ea_status entmax_attn_bwd_noalloc(const ea_shape* shape, const ea_params* params, const void* q,
+                                  const void* k, const void* v, const void* dout,
+                                  const ea_residuals* res, float* dq, float* dk, float* dv,
+                                  void* stream) {
+  Dims d;
+  ea_status st = check_shape(shape, params, &d);
+  if (st != EA_OK) return st;
+  if (d.BH * d.n > (int64_t)EA_NOALLOC_MAX_ROWS) return EA_ERR_UNSUPPORTED;
+  if ((st = prep_bwd_args(shape, params, q, k, v, dout, res, dq, dk, dv, &d)) != EA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipSuccess;
+  float* delta = scratch_for(s, &e);
+  if (!delta) return from_hip(e);
+  for (int stage = 0; stage < 3; ++stage)
+    if ((st = run_bwd_stage(stage, d, params, q, k, v, dout, res, dq, dk, dv, delta, s)) != EA_OK)
+      return st;
+  return EA_OK;
 }
 
 ea_status entmax_rows_fwd(int64_t rows, int32_t n, ea_dtype dtype, const ea_params* params,
