@@ -73,6 +73,12 @@ typedef struct {
  *   k_index    i32   [BH, T, T]    row (b,h,j): K_j ascending in its first k_count entries
  *   stats      i32   [BH, T]       optional (may be NULL): K passes the solver ran for each
  *                                  64-row query block (1 max pass + evaluation passes)
+ *   tau_lo     fp32  [BH, n]       fp32 inputs only (required then; ignored, may be NULL,
+ *                                  for bf16): the threshold is tau + tau_lo to ~fp64
+ *                                  precision.  For alpha not in {1.25, 1.5, 2} the fp32
+ *                                  path refines tau in fp64 and recomputes x - tau in fp64
+ *                                  near the support edge, where u = p^(2-alpha) is
+ *                                  ill-conditioned (Sec. 3.2.2); tau_lo is 0 otherwise.
  */
 typedef struct {
   float* tau;
@@ -83,6 +89,7 @@ typedef struct {
   int32_t* k_count;
   int32_t* k_index;
   int32_t* stats;
+  float* tau_lo;
 } ea_residuals;
 
 /* Byte sizes of every residual buffer and of the workspaces. */
@@ -90,6 +97,7 @@ typedef struct {
   size_t tau, o2, block_mask, q_count, q_index, k_count, k_index, stats;
   size_t ws_fwd; /* workspace entmax_attn_fwd can use: the solver's candidate cache */
   size_t ws_bwd; /* workspace entmax_attn_bwd needs: fp32 [BH, n] for delta */
+  size_t tau_lo; /* fp32 [BH, n] for fp32 inputs, 0 for bf16 */
 } ea_sizes;
 
 /* Library defaults: alpha 1.5, scale 1/sqrt(64), non-causal, max_iter 12,

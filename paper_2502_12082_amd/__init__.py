@@ -53,13 +53,14 @@ class Params(ctypes.Structure):
 
 class ResidualPtrs(ctypes.Structure):
     _fields_ = [(f, ctypes.c_void_p) for f in
-                ("tau", "o2", "block_mask", "q_count", "q_index", "k_count", "k_index", "stats")]
+                ("tau", "o2", "block_mask", "q_count", "q_index", "k_count", "k_index", "stats",
+                 "tau_lo")]
 
 
 class Sizes(ctypes.Structure):
     _fields_ = [(f, ctypes.c_size_t) for f in
                 ("tau", "o2", "block_mask", "q_count", "q_index", "k_count", "k_index", "stats",
-                 "ws_fwd", "ws_bwd")]
+                 "ws_fwd", "ws_bwd", "tau_lo")]
 
 
 _P = ctypes.POINTER
@@ -209,11 +210,15 @@ class Residuals:
         self.k_index = torch.empty(BH * T * T, dtype=torch.int32, device=device).view(BH, T, T)
         self.stats = (torch.empty(z.stats // 4, dtype=torch.int32, device=device)
                       if with_stats else None)
+        # fp32 inputs: the low part of tau (tau + tau_lo to ~fp64 precision)
+        self.tau_lo = (torch.empty(z.tau_lo // 4, dtype=torch.float32, device=device).view(BH, n)
+                       if z.tau_lo else None)
 
     def ptrs(self) -> ResidualPtrs:
         f = lambda t: None if t is None else t.data_ptr()
         return ResidualPtrs(f(self.tau), f(self.o2), f(self.block_mask), f(self.q_count),
-                            f(self.q_index), f(self.k_count), f(self.k_index), f(self.stats))
+                            f(self.q_index), f(self.k_count), f(self.k_index), f(self.stats),
+                            f(self.tau_lo))
 
 
 def _stream_handle(device):
@@ -284,6 +289,8 @@ def _check_residuals(res, shape: Shape, device, need_o2: bool):
     _need(res.k_index, "res.k_index", (BH, T, T), torch.int32, device)
     if res.stats is not None:
         _need(res.stats, "res.stats", (res.sizes.stats // 4,), torch.int32, device)
+    if shape.dtype == EA_F32:
+        _need(res.tau_lo, "res.tau_lo", (BH, n), torch.float32, device)
 
 
 def _check_bytes(ws, name, need_bytes, device):

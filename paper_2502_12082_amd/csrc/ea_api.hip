@@ -100,18 +100,27 @@ void fill_sizes(const Dims& d, ea_sizes* z) {
   z->stats = (size_t)(d.BH * d.T) * 4;
   z->ws_fwd = (size_t)solve_slots(d) * SOLVE_SLOT_BYTES;
   z->ws_bwd = bwd_ws_bytes(d);
+  z->tau_lo = d.dtype == EA_F32 ? (size_t)(d.BH * d.n) * 4 : 0;
 }
 
 bool tensor_ok(const void* p) { return p && aligned(p, 16); }
 bool small_ok(const void* p) { return p && aligned(p, 4); }
 
-ea_status check_tables(const ea_residuals* r) {
+ea_status check_tables(const ea_residuals* r, const Dims& d) {
   if (!r) return EA_ERR_INVALID_ARG;
   if (!small_ok(r->tau) || !r->block_mask || !small_ok(r->q_count) || !small_ok(r->q_index) ||
       !small_ok(r->k_count) || !small_ok(r->k_index))
     return EA_ERR_INVALID_ARG;
   if (r->stats && !aligned(r->stats, 4)) return EA_ERR_INVALID_ARG;
+  if (d.dtype == EA_F32 && !small_ok(r->tau_lo)) return EA_ERR_INVALID_ARG;
   return EA_OK;
+}
+
+// fp64 parameters of the fp32 inputs' refinement, from the fp32 values given
+double c64_of(const ea_params* p) { return ((double)p->alpha - 1.0) * (double)p->scale; }
+double g64_of(const ea_params* p) { return 1.0 / ((double)p->alpha - 1.0); }
+const float* tau_lo_of(const ea_residuals* r, const Dims& d) {
+  return d.dtype == EA_F32 ? r->tau_lo : nullptr;
 }
 
 // HIP error behind the calling thread's most recent EA_ERR_HIP.
@@ -213,7 +222,7 @@ ea_status prep_fwd(const ea_shape* shape, const ea_params* params, const void* q
   if (st != EA_OK) return st;
   if (workspace && !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
   if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(o)) return EA_ERR_INVALID_ARG;
-  if ((st = check_tables(res)) != EA_OK) return st;
+  if ((st = check_tables(res, *d)) != EA_OK) return st;
   if (params->need_bwd && !tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
   return EA_OK;
 }
@@ -234,7 +243,8 @@ ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const
     TauArgs ta{q, k, res->tau, res->block_mask, res->stats, nullptr, nullptr, nullptr, cand,
                TAU_CACHE_CAP, (int)slots,
                (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma, params->causal,
-               params->max_iter, params->tol, gk};
+               params->max_iter, params->tol, gk,
+               const_cast<float*>(tau_lo_of(res, d)), c64_of(params), g64_of(params)};
     return from_hip(launch_tau(ta, d.dtype, (int)d.d, s));
   }
   if (stage == 1) {
@@ -243,7 +253,8 @@ ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const
     return from_hip(launch_compact(ca, s));
   }
   FwdArgs fa{q, k, v, o, params->need_bwd ? res->o2 : nullptr, res->tau, res->q_count,
-             res->q_index, (int)d.BH, (int)d.n, (int)d.T, c, gamma, params->causal, gk};
+             res->q_index, (int)d.BH, (int)d.n, (int)d.T, c, gamma, params->causal, gk,
+             tau_lo_of(res, d), c64_of(params), g64_of(params)};
   return from_hip(launch_fwd(fa, d.dtype, (int)d.d, params->need_bwd != 0, s));
 }
 
@@ -255,7 +266,7 @@ ea_status prep_bwd_args(const ea_shape* shape, const ea_params* params, const vo
   if (st != EA_OK) return st;
   if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(dout)) return EA_ERR_INVALID_ARG;
   if (!tensor_ok(dq) || !tensor_ok(dk) || !tensor_ok(dv)) return EA_ERR_INVALID_ARG;
-  if ((st = check_tables(res)) != EA_OK) return st;
+  if ((st = check_tables(res, *d)) != EA_OK) return st;
   if (!tensor_ok(res->o2)) return EA_ERR_INVALID_ARG;
   return EA_OK;
 }
@@ -283,7 +294,8 @@ ea_status run_bwd_stage(int stage, const Dims& d, const ea_params* params, const
   const float gamma = 1.0f / (params->alpha - 1.0f);
   BwdArgs ba{q, k, v, dout, res->tau, delta, res->q_count, res->q_index, res->k_count,
              res->k_index, dq, dk, dv, (int)d.BH, (int)d.n, (int)d.T, c, gamma,
-             params->scale, params->causal, gamma_kind(params->alpha)};
+             params->scale, params->causal, gamma_kind(params->alpha), tau_lo_of(res, d),
+             c64_of(params), g64_of(params)};
   if (stage == 1) return from_hip(launch_bwd_dkdv(ba, d.dtype, (int)d.d, s));
   return from_hip(launch_bwd_dq(ba, d.dtype, (int)d.d, s));
 }
@@ -401,7 +413,8 @@ ea_status entmax_attn_fwd_dense(const ea_shape* shape, const ea_params* params, 
   const float gamma = 1.0f / (params->alpha - 1.0f);
   TauArgs ta{q, k, tau, nullptr, nullptr, v, o, params->need_bwd ? o2 : nullptr, cand,
              TAU_CACHE_CAP, (int)slots, (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma,
-             params->causal, params->max_iter, params->tol, gamma_kind(params->alpha)};
+             params->causal, params->max_iter, params->tol, gamma_kind(params->alpha), nullptr,
+             c64_of(params), g64_of(params)};
   return from_hip(launch_tau_fused(ta, d.dtype, (int)d.d, static_cast<hipStream_t>(stream)));
 }
 

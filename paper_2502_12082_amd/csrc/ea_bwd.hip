@@ -85,6 +85,7 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
   const float* taug = a.tau + (size_t)bh * n;
   const float* delg = a.delta + (size_t)bh * n;
   const float c = a.c, g = a.gamma;
+  constexpr bool PRECISE = precise_path<E, GK>();
 
   typename M::frag kf[KS], vf[KS];
 #pragma unroll
@@ -135,7 +136,21 @@ __global__ __launch_bounds__(BWD_NT) void dkdv_kernel(BwdArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int r = 4 * g4 + e;
-        const float zp = relu_z(c, s[r], tq[e]);
+        float zp;
+        if constexpr (PRECISE) {
+          // fp64 z near the support edge (ea_common.h); invalid pairs hold -inf
+          const int i = i0 + crow(r);
+          const bool ok = i < n && j < n;
+          const float band = PRECISE_BAND * fmaxf(1.f, fabsf(tq[e]));
+          const float raw = fmaf(c, s[r], -tq[e]);
+          double t64 = tq[e];
+          if (ok && fabsf(raw) < band && a.tau_lo) t64 += (double)a.tau_lo[(size_t)bh * n + i];
+          zp = precise_relu_z<D>(ok, c, s[r], tq[e], band, t64,
+                                 reinterpret_cast<const float*>(Qg) + (size_t)i * D,
+                                 reinterpret_cast<const float*>(Kg) + (size_t)j * D, a.c64);
+        } else {
+          zp = relu_z(c, s[r], tq[e]);
+        }
         float u;
         Gamma<GK>::pu(zp, g, p[r], u);
         dsv[r] = u * (dp[r] - dq4[e]);
@@ -515,6 +530,11 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
   const float tau = i < n ? a.tau[(size_t)bh * n + i] : 0.f;
   const float del = i < n ? a.delta[(size_t)bh * n + i] : 0.f;
   const float c = a.c, g = a.gamma;
+  constexpr bool PRECISE = precise_path<E, GK>();
+  // fp32 inputs, general alpha: fp64 z near the support edge (ea_common.h)
+  [[maybe_unused]] const double tau64 =
+      (double)tau + (PRECISE && a.tau_lo && i < n ? (double)a.tau_lo[(size_t)bh * n + i] : 0.0);
+  [[maybe_unused]] const float band = PRECISE_BAND * fmaxf(1.f, fabsf(tau));
 
   typename M::frag qf[KS], df[KS];
 #pragma unroll
@@ -574,7 +594,14 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
     float dsv[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float zp = relu_z(c, s[r], tau);
+      float zp;
+      if constexpr (PRECISE) {
+        zp = precise_relu_z<D>(i < n, c, s[r], tau, band, tau64,
+                               reinterpret_cast<const float*>(Qg) + (size_t)i * D,
+                               reinterpret_cast<const float*>(Kg) + (size_t)(j0 + crow(r)) * D, a.c64);
+      } else {
+        zp = relu_z(c, s[r], tau);
+      }
       float p, u;
       Gamma<GK>::pu(zp, g, p, u);
       dsv[r] = u * (dp[r] - del);

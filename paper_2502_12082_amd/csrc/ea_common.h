@@ -26,6 +26,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace ea {
 
 constexpr int BLK = 64;  // mask block edge (rows and columns)
@@ -366,6 +368,56 @@ __device__ __forceinline__ int in_support(float zp) {
 #else
   return zp > 0.f ? 1 : 0;
 #endif
+}
+
+// ------------------------------------- fp32 inputs with a general alpha
+//
+// For gamma = 1/(alpha-1) below 2 (alpha > 1.5) u = z^(gamma-1) has an
+// unbounded slope as z -> 0+ (Sec. 3.2.2, App. A.2).  An fp32 score carries
+// a rounding error of ~1e-7 |x| from its fp32 accumulation, and u of an entry
+// that close to the support edge can then be off by far more than the fp32
+// tolerance; tau solved on fp32 scores moves the whole edge by as much.  With
+// fp32 inputs and a general alpha the kernels therefore take z = x - tau in
+// fp64 for every entry within PRECISE_BAND * max(1, |tau|) of the edge: the
+// products of fp32 inputs are exact in fp64, and tau carries a low part
+// (tau + tau_lo) that the solver refines in fp64.
+template <typename E, int GK>
+constexpr bool precise_path() {
+  return std::is_same<E, float>::value && GK == 0;
+}
+constexpr float PRECISE_BAND = 0.01f;
+
+// (alpha-1) * scale * <q, k> in fp64 for fp32 rows q, k of length D (16-byte
+// aligned); every product is exact in fp64.
+template <int D>
+__device__ __forceinline__ double exact_x(const float* q, const float* k, double c64) {
+  double a0 = 0.0, a1 = 0.0;
+#pragma unroll 4
+  for (int t = 0; t < D; t += 4) {
+    const f32x4 x = *reinterpret_cast<const f32x4*>(q + t);
+    const f32x4 y = *reinterpret_cast<const f32x4*>(k + t);
+    a0 = fma((double)x[0], (double)y[0], a0);
+    a1 = fma((double)x[1], (double)y[1], a1);
+    a0 = fma((double)x[2], (double)y[2], a0);
+    a1 = fma((double)x[3], (double)y[3], a1);
+  }
+  return c64 * (a0 + a1);
+}
+
+// [x - tau]_+ clamped to [0, 1] (as relu_z) for a valid entry of row q and
+// key k with fp32 score s: within the band of the edge from fp64 x and the
+// fp64 tau64 = tau + tau_lo, elsewhere in fp32.  `ok` is false for rows past
+// the end (nothing is read then).
+template <int D>
+__device__ __forceinline__ float precise_relu_z(bool ok, float c, float s, float tau, float band,
+                                                double tau64, const float* q, const float* k,
+                                                double c64) {
+  const float raw = fmaf(c, s, -tau);
+  if (ok && fabsf(raw) < band) {
+    const double z = exact_x<D>(q, k, c64) - tau64;
+    return (float)fmin(fmax(z, 0.0), 1.0);
+  }
+  return __builtin_amdgcn_fmed3f(raw, 0.f, 1.f);
 }
 
 // GK = gamma for the integer cases 1 (alpha = 2), 2 (alpha = 1.5),

@@ -102,6 +102,11 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
   const E* V = static_cast<const E*>(a.v) + head;
   const float tau = i < n ? a.tau[(size_t)bh * n + i] : 0.f;
   const float c = a.c, g = a.gamma;
+  constexpr bool PRECISE = precise_path<E, GK>();
+  // fp32 inputs, general alpha: fp64 z near the support edge (ea_common.h)
+  [[maybe_unused]] const double tau64 =
+      (double)tau + (PRECISE && a.tau_lo && i < n ? (double)a.tau_lo[(size_t)bh * n + i] : 0.0);
+  [[maybe_unused]] const float band = PRECISE_BAND * fmaxf(1.f, fabsf(tau));
 
   typename M::frag qf[KS];
 #pragma unroll
@@ -156,7 +161,14 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
     float p[16], u[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float zp = relu_z(c, s[r], tau);
+      float zp;
+      if constexpr (PRECISE) {
+        zp = precise_relu_z<D>(i < n, c, s[r], tau, band, tau64,
+                               reinterpret_cast<const float*>(Q) + (size_t)i * D,
+                               reinterpret_cast<const float*>(K) + (size_t)(j0 + crow(r)) * D, a.c64);
+      } else {
+        zp = relu_z(c, s[r], tau);
+      }
       if constexpr (TRAIN) {
         Gamma<GK>::pu(zp, g, p[r], u[r]);
         usum += u[r];

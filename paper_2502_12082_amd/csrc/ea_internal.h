@@ -17,11 +17,10 @@ constexpr int MAX_KEY_BLOCKS = MAX_SEQLEN / 64;
 int gamma_kind(float alpha);
 
 // One cached score of the solver: the raw score s = <q_i, k_j> (the solver
-// forms x - tau from it exactly as in a streamed evaluation) and the key
-// block of j.
+// forms x - tau from it exactly as in a streamed evaluation) and the key j.
 struct alignas(8) CandEntry {
   float s;
-  int32_t kb;
+  int32_t j;  // key index; its key block is j / 64
 };
 
 // Workgroup geometry (rows and threads per workgroup) of the masked path's
@@ -52,6 +51,11 @@ struct TauArgs {
   int causal, max_iter;
   float tol;
   int gk;             // gamma_kind(alpha)
+  // fp32 inputs, general alpha: tau is refined in fp64 and written as
+  // tau + tau_lo ([BH, n]); c64, g64 are (alpha - 1) * scale and 1/(alpha - 1)
+  // in fp64 from the same fp32 parameters
+  float* tau_lo;
+  double c64, g64;
 };
 
 struct CompactArgs {
@@ -73,6 +77,8 @@ struct FwdArgs {
   float c, gamma;
   int causal;
   int gk;
+  const float* tau_lo;  // fp32 inputs, general alpha: low part of tau (or null: 0)
+  double c64, g64;
 };
 
 struct BwdArgs {
@@ -91,6 +97,8 @@ struct BwdArgs {
   float c, gamma, scale;
   int causal;
   int gk;
+  const float* tau_lo;  // fp32 inputs, general alpha: low part of tau (or null: 0)
+  double c64, g64;
 };
 
 struct DeltaArgs {

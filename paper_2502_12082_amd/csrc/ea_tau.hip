@@ -309,11 +309,11 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
       // lo / c (a superset of the entries is harmless).
       const float s_lo0 = lo / c;
       const float s_lo = row_ok ? s_lo0 - 1e-6f * fmaxf(fabsf(s_lo0), 1.f / c) : INFINITY;
-      auto fill_tile = [&](const f32x16& s, int kb) {
+      auto fill_tile = [&](const f32x16& s, int jb) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           if (s[r] > s_lo) {
-            if (cc < a.cap) mine[(size_t)cc * TAU_NT] = CandEntry{s[r], kb};
+            if (cc < a.cap) mine[(size_t)cc * TAU_NT] = CandEntry{s[r], jb + crow(r)};
             ++cc;
           }
         }
@@ -344,8 +344,8 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
           scores(kt, s0, s1);
           if (k0 == 2) mask_tile(s0, j0);
           if (k1 == 2) mask_tile(s1, j0 + 32);
-          if (k0) fill_tile(s0, kb);
-          if (k1) fill_tile(s1, kb);
+          if (k0) fill_tile(s0, j0);
+          if (k1) fill_tile(s1, j0 + 32);
         });
         fill_done();
       }
@@ -368,8 +368,8 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
             eval_tile(s0);
             eval_tile(s1);
             if (fill_now) {
-              fill_tile(s0, kb);
-              fill_tile(s1, kb);
+              fill_tile(s0, j0);
+              fill_tile(s1, j0 + 32);
             }
           } else if (k0 != 0 || k1 != 0) {
             f32x16 s0, s1;
@@ -379,8 +379,8 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
             if (k0) eval_tile(s0);
             if (k1) eval_tile(s1);
             if (fill_now) {
-              if (k0) fill_tile(s0, kb);
-              if (k1) fill_tile(s1, kb);
+              if (k0) fill_tile(s0, j0);
+              if (k1) fill_tile(s1, j0 + 32);
             }
           }
           if (fill_now && cc > a.cap) fill_full = 1;
@@ -778,11 +778,11 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   auto entry_idx = [&](int e, int gq) {
     return (uint32_t)e * ENTRY_STEP + (uint32_t)(gq * SV_NT + (int)threadIdx.x);
   };
-  auto put = [&](uint32_t idx, float sv, int kbv) { cache[idx] = CandEntry{sv, kbv}; };
+  auto put = [&](uint32_t idx, float sv, int jv) { cache[idx] = CandEntry{sv, jv}; };
   // the same store at a 32-bit byte offset from the slot base (a wave-uniform
   // base plus a per-lane offset needs no 64-bit address arithmetic)
-  auto put_at = [&](uint32_t byte_off, float sv, int kbv) {
-    *reinterpret_cast<CandEntry*>(reinterpret_cast<char*>(cache) + byte_off) = CandEntry{sv, kbv};
+  auto put_at = [&](uint32_t byte_off, float sv, int jv) {
+    *reinterpret_cast<CandEntry*>(reinterpret_cast<char*>(cache) + byte_off) = CandEntry{sv, jv};
   };
   auto wave_max = [&](int v) {
 #pragma unroll
@@ -793,15 +793,15 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // up to the wave's longest list cmax rounded up to a multiple of 8.  That
   // stays inside the slot (cmax <= cap, and cap is a multiple of 8); entries
   // past this thread's own count are stale and never used.
-  // use(score, key block) for each entry of list gq.
-  auto scan_kb = [&](int gq, auto&& use) {
+  // use(score, key) for each entry of list gq.
+  auto scan_entries = [&](int gq, auto&& use) {
     for (int e0 = 0; e0 < cmax[gq]; e0 += 8) {
       CandEntry ce[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) ce[u] = cache[entry_idx(e0 + u, gq)];
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        if (e0 + u < cc[gq]) use(ce[u].s, ce[u].kb);
+        if (e0 + u < cc[gq]) use(ce[u].s, ce[u].j);
     }
   };
   // The scores of both lists for an evaluation: sixteen independent 4-byte
@@ -827,7 +827,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   auto filter = [&](int gq, float sb) {
     cmax[gq] = wave_max(cc[gq]);
     int k = 0;
-    scan_kb(gq, [&](float sv, int kv) {
+    scan_entries(gq, [&](float sv, int kv) {
       if (sv > sb) put(entry_idx(k++, gq), sv, kv);
     });
     cc[gq] = k;
@@ -964,7 +964,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 #pragma unroll
             for (int r = r0; r < r0 + 4; ++r) {
               if (t[r] > sb[gq]) {
-                put_at(off, t[r], kb);
+                put_at(off, t[r], kb * BLK + 32 * h + crow(r));
                 off += STEP_BYTES;
               }
             }
@@ -1073,11 +1073,11 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       const float t0 = lo[gq] / c;
       s_lo[gq] = row_ok[gq] ? t0 - 1e-6f * fmaxf(fabsf(t0), 1.f / c) : INFINITY;
     }
-    auto fill_tile = [&](const f32x16& s, int gq, int kb) {
+    auto fill_tile = [&](const f32x16& s, int gq, int jb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         if (s[r] > s_lo[gq]) {
-          if (cc[gq] < a.cap) put(entry_idx(cc[gq], gq), s[r], kb);
+          if (cc[gq] < a.cap) put(entry_idx(cc[gq], gq), s[r], jb + crow(r));
           ++cc[gq];
         }
       }
@@ -1105,7 +1105,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         for (int h = 0; h < 2; ++h)
 #pragma unroll
           for (int gq = 0; gq < 2; ++gq)
-            if (k[h][gq]) fill_tile(s[h][gq], gq, kb);
+            if (k[h][gq]) fill_tile(s[h][gq], gq, kb * BLK + 32 * h);
       });
       ++passes;
       fill_done();
@@ -1204,21 +1204,111 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     if (stop) break;
   }
 
-  if (lane < 32) {
+  if constexpr (precise_path<E, GK>()) {
+    // ---- fp32 inputs, general alpha (ea_common.h): tau refined in fp64 and
+    // written as tau + tau_lo, and the mask written at the refined tau.  Every
+    // entry above the lower edge of the band is taken with its fp64 score;
+    // Newton steps on f (Eq. 3, 6) from the fp32 tau, which is already close
+    // to the root, square the error each time.  The result stays in the
+    // bracket, widened by the rounding of its fp32 ends.
+    const float* Qf = reinterpret_cast<const float*>(Q);
+    const float* Kf = reinterpret_cast<const float*>(K);
+    float band[2];
+    double t64[2];
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq)
-      if (row_ok[gq]) a.tau[(size_t)bh * n + qi[gq]] = tau[gq];
-  }
-
-  if (cached) {
-    // mask bits at the returned tau from the cached entries
+    for (int gq = 0; gq < 2; ++gq) {
+      band[gq] = PRECISE_BAND * fmaxf(1.f, fabsf(tau[gq]));
+      t64[gq] = tau[gq];
+    }
+    // use(group, fp32 score, key) for every valid entry of this lane's rows:
+    // from the lists when they hold every candidate, else from a K pass
+    auto visit = [&](auto&& use) {
+      if (cached) {
+#pragma unroll
+        for (int gq = 0; gq < 2; ++gq) scan_entries(gq, [&](float sv, int jv) { use(gq, sv, jv); });
+      } else {
+        stream([&](int kb, const E* kt) {
+          f32x16 s[2][2];
+          int k[2][2];
+          if (!block(kb, kt, s, k)) return;
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int gq = 0; gq < 2; ++gq)
+              if (k[h][gq]) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) use(gq, s[h][gq][r], kb * BLK + 32 * h + crow(r));
+              }
+        });
+        ++passes;
+      }
+    };
+    // fp64 z of an entry, or -1 for one below the band (outside the support)
+    auto z64 = [&](int gq, float sv, int jv) -> double {
+      const float raw = fmaf(c, sv, -tau[gq]);
+      if (!(raw > -band[gq])) return -1.0;
+      return exact_x<D>(Qf + (size_t)qi[gq] * D, Kf + (size_t)jv * D, a.c64) - t64[gq];
+    };
+    for (int it = 0; it < 3; ++it) {
+      double s0[2] = {0.0, 0.0}, s1[2] = {0.0, 0.0};
+      visit([&](int gq, float sv, int jv) {
+        if (!row_ok[gq]) return;
+        const double z = z64(gq, sv, jv);
+        if (z > 0.0) {
+          s0[gq] += pow(z, a.g64);
+          s1[gq] += pow(z, a.g64 - 1.0);
+        }
+      });
+#pragma unroll
+      for (int gq = 0; gq < 2; ++gq) {
+        s0[gq] += __shfl_xor(s0[gq], 32);
+        s1[gq] += __shfl_xor(s1[gq], 32);
+        if (row_ok[gq] && s1[gq] > 0.0) {
+          const double slack = 1e-5 * fmax(1.0, fmax(fabs((double)lo[gq]), fabs((double)hi[gq])));
+          const double tn = t64[gq] + (s0[gq] - 1.0) / (a.g64 * s1[gq]);
+          t64[gq] = fmin(fmax(tn, (double)lo[gq] - slack), (double)hi[gq] + slack);
+        }
+      }
+    }
+    if (lane < 32) {
+#pragma unroll
+      for (int gq = 0; gq < 2; ++gq)
+        if (row_ok[gq]) {
+          const float th = (float)t64[gq];
+          a.tau[(size_t)bh * n + qi[gq]] = th;
+          a.tau_lo[(size_t)bh * n + qi[gq]] = (float)(t64[gq] - (double)th);
+        }
+    }
     for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
     __syncthreads();
+    visit([&](int gq, float sv, int jv) {
+      if (!row_ok[gq]) return;
+      const float raw = fmaf(c, sv, -tau[gq]);
+      if (raw >= band[gq] || z64(gq, sv, jv) > 0.0) {
+        const int kv = jv >> 6;
+        atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+      }
+    });
+  } else {
+    if (lane < 32) {
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq)
-      scan_kb(gq, [&](float sv, int kv) {
-        if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
-      });
+      for (int gq = 0; gq < 2; ++gq)
+        if (row_ok[gq]) {
+          a.tau[(size_t)bh * n + qi[gq]] = tau[gq];
+          if (std::is_same<E, float>::value) a.tau_lo[(size_t)bh * n + qi[gq]] = 0.f;
+        }
+    }
+    if (cached) {
+      // mask bits at the returned tau from the cached entries
+      for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int gq = 0; gq < 2; ++gq)
+        scan_entries(gq, [&](float sv, int jv) {
+          const int kv = jv >> 6;
+          if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+        });
+    }
   }
   __syncthreads();
   if (!wave_ok) return;

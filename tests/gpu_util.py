@@ -58,6 +58,8 @@ def run_gpu(inp: dict, alpha: float, scale: float, causal: bool, bwd: bool, max_
     torch.cuda.synchronize()
     out.update(o=o.float(), tau=res.tau, mask=res.block_mask, q_count=res.q_count,
                q_index=res.q_index, k_count=res.k_count, k_index=res.k_index, stats=res.stats)
+    if res.tau_lo is not None:
+        out["tau_lo"] = res.tau_lo
     if bwd:
         out["o2"] = res.o2
     host = {}
@@ -76,12 +78,20 @@ def run_gpu(inp: dict, alpha: float, scale: float, causal: bool, bwd: bool, max_
     return host
 
 
+def abi_param(x: float) -> float:
+    """The value the C ABI receives for alpha or scale: they are fp32 fields,
+    so the oracle computes with the same fp32-rounded numbers."""
+    return float(np.float32(x))
+
+
 def oracle_head(inp: dict, bh: int, alpha, scale, causal, bwd, rows=None, cols=None,
                 block_rows=None):
     """Oracle outputs for head bh.  rows/cols=None: every row/column; otherwise
     only those rows (tau, O, O2, dQ) and columns (dK, dV) are computed, plus
     whatever rows the listed columns depend on.  block_rows: 64-row query
-    blocks whose mask margins to compute (None with rows=None: all)."""
+    blocks whose mask margins to compute (None with rows=None: all).  alpha
+    and scale are taken as the fp32 values the GPU path is given."""
+    alpha, scale = abi_param(alpha), abi_param(scale)
     B, H, n, d = inp["q"].shape
     b, h = divmod(bh, H)
     q = inp["q"].f64()[b, h]
@@ -131,6 +141,8 @@ def check_head(gpu: dict, ref: dict, bh: int, dtype: str, label: str, rows=None,
     r = np.arange(n) if rows is None else np.asarray(sorted(rows))
     errs = {}
     tr, tg = ref["tau"][r], gpu["tau"][bh][r]
+    if "tau_lo" in gpu:
+        tg = tg + gpu["tau_lo"][bh][r]
     errs["tau_rel"] = float(np.max(np.abs(tg - tr) / np.maximum(1.0, np.abs(tr))))
     assert errs["tau_rel"] <= TAU_REL, (label, "tau", errs)
     errs["o"] = maxabs(gpu["o"][bh][r], ref["o"][r])
@@ -185,9 +197,10 @@ def check_mask_self(gpu: dict, bh: int, block_rows, label):
     skipped).  Returns the number of blocks inside that band."""
     inp = gpu["inputs"]
     alpha, scale, causal = gpu["params"]
+    alpha, scale = abi_param(alpha), abi_param(scale)
     B, H, n, d = inp["q"].shape
     b, h = divmod(bh, H)
-    tau = gpu["tau"][bh]
+    tau = gpu["tau"][bh] + (gpu["tau_lo"][bh] if "tau_lo" in gpu else 0.0)
     margin = oracle.head_block_margin(inp["q"].f64()[b, h], inp["k"].f64()[b, h], alpha, scale,
                                       causal, tau, block_rows=block_rows)
     mask = gpu["mask"][bh]
