@@ -62,7 +62,17 @@ def traffic_path(kernel):
 def measured_traffic(kernel):
     """HBM bytes per launch of `kernel` from its committed counter summary, or
     None when there is none or its sources have changed since."""
-    path = traffic_path(kernel)
+    f = summary_fields(traffic_path(kernel), kernel)
+    return None if f is None else float(f["hbm_bytes_per_launch"])
+
+
+def mfma_path(kernel):
+    return os.path.join(ROOT, "profiles", "mfma_%s.md" % kernel)
+
+
+def summary_fields(path, kernel):
+    """The `- key: value` lines of a committed counter summary, or None when
+    there is none or the kernel's sources have changed since it was taken."""
     if not os.path.exists(path):
         return None
     fields = {}
@@ -72,7 +82,96 @@ def measured_traffic(kernel):
             fields[key.strip().strip("`")] = val.strip().strip("`")
     if fields.get("sources_sha256") != sources_sha256(kernel):
         return None
-    return float(fields["hbm_bytes_per_launch"])
+    return fields
+
+
+def measured_mfma(kernel):
+    """(MFMA-busy fraction, executed MFMA FLOPs per launch) of `kernel` from its
+    committed rocprofv3 counter summary, or None."""
+    f = summary_fields(mfma_path(kernel), kernel)
+    if f is None:
+        return None
+    return float(f["mfma_busy"]), float(f["mfma_flops_per_launch"])
+
+
+def write_mfma(pmc_csv, command, head_dim=128):
+    """One summary per kernel from a rocprofv3 --pmc run of MfmaUtil and
+    SQ_INSTS_VALU_MFMA_MOPS_BF16: MfmaUtil = busy cycles of the MFMA units over
+    GRBM_GUI_ACTIVE x SIMDs (rocprofv3's derived counter), and the executed
+    bf16 MFMA FLOPs per dispatch (512 per MOPS count)."""
+    import csv
+    import collections
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for row in csv.DictReader(open(pmc_csv)):
+        vals[row["Kernel_Name"]][row["Counter_Name"]].append(float(row["Counter_Value"]))
+    for kernel, frag in PROFILE_NAMES.items():
+        names = [k for k in vals if frag in k and headline_instance(k, head_dim)]
+        if not names:
+            continue
+        util = [v for k in names for v in vals[k]["MfmaUtil"]]
+        mops = [v for k in names for v in vals[k]["SQ_INSTS_VALU_MFMA_MOPS_BF16"]]
+        busy = sum(util) / len(util) / 100.0
+        flops = sum(mops) / len(mops) * 512.0
+        with open(mfma_path(kernel), "w") as fh:
+            fh.write("# MFMA utilisation of `%s` (rocprofv3 MfmaUtil, SQ_INSTS_VALU_MFMA_MOPS_BF16)\n\n"
+                     % frag)
+            fh.write("Commands (repository root on an MI355X; `cd /tmp && export TMPDIR=/tmp` "
+                     "first):\n\n```\n%s\n```\n\n" % command)
+            fh.write("MfmaUtil is rocprofv3's derived counter: SQ_VALU_MFMA_BUSY_CYCLES summed over "
+                     "the SIMDs / (GRBM_GUI_ACTIVE x SIMD count) x 100, i.e. the fraction of the "
+                     "dispatch's cycles the matrix units were busy.  Executed FLOPs are "
+                     "512 per SQ_INSTS_VALU_MFMA_MOPS_BF16 count (the hi/lo operand splits "
+                     "included).\n\n")
+            fh.write("| dispatches | MfmaUtil % (mean) | MFMA MOPS (mean) |\n|---|---|---|\n")
+            fh.write("| %d | %.2f | %.0f |\n\n" % (len(util), busy * 100.0, sum(mops) / len(mops)))
+            fh.write("- mfma_busy: %.4f\n" % busy)
+            fh.write("- mfma_flops_per_launch: %.0f\n" % flops)
+            fh.write("- sources_sha256: `%s`\n" % sources_sha256(kernel))
+        print("wrote %s: MFMA busy %.1f%%, %.3e FLOP per launch" % (mfma_path(kernel),
+                                                                    busy * 100, flops))
+
+
+def write_kernel_stats(stats_csv, bench_json, out_md, command):
+    """profiles/<out_md>: rocprofv3's per-kernel statistics of a profiled run
+    next to the HIP-event kernel times of an unprofiled run of the same
+    command (its JSON line), with the roofline fraction each timing gives."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    line = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    flops = {k: v["tflops"] * v["ms"] * 1e9 for k, v in line["kernels"].items()}
+    with open(out_md, "w") as fh:
+        fh.write("# rocprofv3 kernel statistics: %s\n\n" % line["config"]["workload"])
+        fh.write("Commands (repository root on an MI355X; `cd /tmp && export TMPDIR=/tmp` "
+                 "first):\n\n```\n%s\n```\n\n" % command)
+        fh.write("| kernel | calls | average us | % of GPU time |\n|---|---|---|---|\n")
+        avg = {}
+        for r in rows:
+            name = r["Name"]
+            short = name if len(name) < 90 else name[:87] + "..."
+            fh.write("| `%s` | %s | %.1f | %.2f |\n" % (short, r["Calls"],
+                                                     float(r["AverageNs"]) / 1e3,
+                                                     float(r["Percentage"])))
+            for kernel, frag in PROFILE_NAMES.items():
+                if frag in name and headline_instance(name, line["config"]["head_dim"]):
+                    avg[kernel] = float(r["AverageNs"]) / 1e6
+        fh.write("\nSame kernels, HIP-event times of the unprofiled run (`python bench.py` with "
+                 "the arguments above, no profiler attached), and the fraction of the 2.5 PFLOP/s "
+                 "bf16 peak that each timing gives for the kernel's algorithmic FLOPs:\n\n")
+        fh.write("| kernel | algorithmic TFLOP per launch | profiled ms | frac | unprofiled ms "
+                 "| frac |\n|---|---|---|---|---|---|\n")
+        for kernel in PROFILE_NAMES:
+            if kernel not in avg:
+                continue
+            t = line["kernels"][kernel]["ms"]
+            f = flops[kernel]
+            fh.write("| %s | %.4f | %.4f | %.3f | %.4f | %.3f |\n" % (
+                kernel, f / 1e12, avg[kernel], f / (avg[kernel] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                t, f / (t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS))
+        fh.write("\nUnprofiled run: %.4f ms per step (p10 %.4f, p90 %.4f).  The profiler's "
+                 "kernel trace makes kernels run a few percent slower; the JSON line's "
+                 "`roofline.frac` uses the unprofiled timing.\n"
+                 % (line["ms_per_step"], line["step_ms"]["p10"], line["step_ms"]["p90"]))
+    print("wrote %s" % out_md)
 
 
 def headline_instance(name, head_dim):
@@ -166,6 +265,12 @@ def parse():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed region, one plain device copy of this many MiB "
                          "(the reference dispatch for HBM counter scaling)")
+    ap.add_argument("--kernel-stats-from", nargs=3, metavar=("STATS_CSV", "BENCH_JSON", "OUT_MD"),
+                    help="write a kernel-statistics summary from a rocprofv3 --kernel-trace "
+                         "--stats run and an unprofiled run's JSON line, then exit")
+    ap.add_argument("--mfma-from", metavar="PMC_CSV",
+                    help="write profiles/mfma_<kernel>.md from a rocprofv3 --pmc MfmaUtil "
+                         "SQ_INSTS_VALU_MFMA_MOPS_BF16 run of this script, then exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic_<kernel>.md from two rocprofv3 --pmc runs "
                          "(FETCH_SIZE, WRITE_SIZE) of this script with --calib-copy-mib, then exit")
@@ -242,11 +347,16 @@ class Runner:
         kern = None
         if per_kernel:
             kern = {name: 0.0 for name in KERNELS}
+            per_step = []
             for i in range(steps):
                 ev = self.events[i]
                 for j, name in enumerate(KERNELS):
                     kern[name] += ev[j].elapsed_time(ev[j + 1])
+                per_step.append(ev[0].elapsed_time(ev[len(KERNELS)]))
             kern = {k_: v_ / steps for k_, v_ in kern.items()}
+            q = np.percentile(per_step, [10, 50, 90])
+            kern["_steps"] = {"p10": round(float(q[0]), 4), "median": round(float(q[1]), 4),
+                              "p90": round(float(q[2]), 4)}
         return total_ms / steps, wall, kern
 
     def work(self):
@@ -260,7 +370,8 @@ class Runner:
         else:
             n_valid = BH * T * T
         n_act = int(self.res.q_count.sum().item())
-        stats = self.res.stats.cpu().numpy().astype(np.int64).reshape(BH, T)
+        planes = self.res.stats.cpu().numpy().astype(np.int64).reshape(2, BH, T)
+        stats, evals = planes[0], planes[1]
         # valid 64x64 blocks each query block streams per solver pass
         per_qb = np.arange(1, T + 1) if self.params.causal else np.full(T, T)
         # The solver's work is its K passes: the max pass and the evaluation
@@ -270,26 +381,46 @@ class Runner:
         solver_blocks = float((stats * per_qb[None, :]).sum())
         flops = {"tau_solve": solver_blocks * f_blk, "compact": 0.0, "bwd_delta": 0.0}
         for k_, m in PRODUCTS_PER_ACTIVE.items():
+            # the forward without a backward to follow forms S and P V only
+            if k_ == "fwd_sparse" and not self.bwd:
+                m = 2
             flops[k_] = m * n_act * f_blk
         dense = 14.0 * n * n * d * BH * (0.5 if self.params.causal else 1.0)
         return {"n_valid": n_valid, "n_act": n_act, "block_density": n_act / n_valid,
                 "passes_mean": float(stats.mean()), "passes_max": int(stats.max()),
+                "evals_mean": float(evals.mean()), "evals_max": int(evals.max()),
                 "flops": flops, "dense_flops": dense, "mask_nnz": int(mask.sum())}
+
+    def _sampled_z(self, rows):
+        """x - tau (fp64, from the input values and the returned tau) on
+        `rows` sampled rows of head 0; invalid pairs hold -1."""
+        q = self.inp["q"].f64()[0, 0]
+        k = self.inp["k"].f64()[0, 0]
+        tau = self.res.tau[0].cpu().numpy().astype(np.float64)
+        if self.res.tau_lo is not None:
+            tau = tau + self.res.tau_lo[0].cpu().numpy().astype(np.float64)
+        idx = np.linspace(0, self.n - 1, rows).astype(int)
+        a, sc = float(np.float32(self.params.alpha)), float(np.float32(self.params.scale))
+        z = (a - 1) * sc * (q[idx] @ k.T) - tau[idx, None]
+        if self.params.causal:
+            z = np.where(np.arange(self.n)[None, :] <= idx[:, None], z, -1.0)
+        return idx, z
 
     def zero_fraction(self, rows=64):
         """Fraction of zero probabilities on sampled rows of head 0, from the
         returned tau (host numpy; a statistic, not part of the timed path)."""
-        q = self.inp["q"].f64()[0, 0]
-        k = self.inp["k"].f64()[0, 0]
-        tau = self.res.tau[0].cpu().numpy().astype(np.float64)
-        idx = np.linspace(0, self.n - 1, rows).astype(int)
-        x = (self.params.alpha - 1) * self.params.scale * (q[idx] @ k.T) - tau[idx, None]
-        if self.params.causal:
-            x = np.where(np.arange(self.n)[None, :] <= idx[:, None], x, -1.0)
-            valid = (idx + 1).sum()
-        else:
-            valid = rows * self.n
-        return 1.0 - float((x > 0).sum()) / valid
+        idx, z = self._sampled_z(rows)
+        valid = (idx + 1).sum() if self.params.causal else rows * self.n
+        return 1.0 - float((z > 0).sum()) / valid
+
+    def sum_p_error(self, rows=64):
+        """max |sum_j p_ij - 1| over sampled rows of head 0 at the returned tau:
+        f(tau) of Eq. 3, the residual Algorithm 1's output leaves (O is not
+        renormalised)."""
+        _, z = self._sampled_z(rows)
+        g = 1.0 / (float(np.float32(self.params.alpha)) - 1.0)
+        p = np.where(z > 0, np.maximum(z, 0.0) ** g, 0.0)
+        return float(np.max(np.abs(p.sum(1) - 1.0)))
 
 
 PEAK_HBM_GBS = 8000.0
@@ -331,17 +462,31 @@ def rows_bench(steps=20, warmup=3, rows=8192, n=8192, alpha=1.5):
 
 def dense_mode_bench(run, steps=5, warmup=2):
     """The no-mask mode (fused tau + O forward, table-free backward) on the
-    headline workload: ms per fwd+bwd step and dense-equivalent TFLOP/s."""
+    headline workload: ms per fwd+bwd step and dense-equivalent TFLOP/s.  All
+    buffers are allocated before the timed loop, which makes only the two C
+    ABI calls per step."""
+    import ctypes
     import torch
     import paper_2502_12082_amd as ea
     q, k, v, do = run.q, run.k, run.v, run.do
     p = run.params
-    kw = dict(alpha=p.alpha, scale=p.scale, causal=bool(p.causal))
+    o = torch.empty_like(q)
+    tau = torch.empty((run.B * run.H, run.n), dtype=torch.float32, device=q.device)
+    f32 = lambda: torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    o2, dq, dk, dv = f32(), f32(), f32(), f32()
     ws = ea.forward_workspace(run.res, q.device)
+    wsb = torch.empty(run.res.sizes.ws_bwd // 4 + 4, dtype=torch.float32, device=q.device)
+    shape, stream = run.shape, torch.cuda.current_stream().cuda_stream
+    ptr = lambda t: t.data_ptr()
 
     def step():
-        o, tau, o2 = ea.forward_dense(q, k, v, need_bwd=True, workspace=ws, **kw)
-        ea.backward_dense(q, k, v, do, tau, o2, **kw)
+        ea._check(ea._lib.entmax_attn_fwd_dense(
+            ctypes.byref(shape), ctypes.byref(p), ptr(q), ptr(k), ptr(v), ptr(o), ptr(tau),
+            ptr(o2), ptr(ws), ws.numel(), stream), "entmax_attn_fwd_dense")
+        ea._check(ea._lib.entmax_attn_bwd_dense(
+            ctypes.byref(shape), ctypes.byref(p), ptr(q), ptr(k), ptr(v), ptr(do), ptr(tau),
+            ptr(o2), ptr(dq), ptr(dk), ptr(dv), ptr(wsb), wsb.numel() * 4, stream),
+            "entmax_attn_bwd_dense")
 
     for _ in range(warmup):
         step()
@@ -354,8 +499,7 @@ def dense_mode_bench(run, steps=5, warmup=2):
     torch.cuda.synchronize()
     ms = a.elapsed_time(b) / steps
     dense = 14.0 * run.n * run.n * run.d * run.B * run.H * (0.5 if p.causal else 1.0)
-    return {"ms_per_step": round(ms, 4), "tflops_dense_equiv": round(dense / (ms * 1e-3) / 1e12, 3),
-            "note": "includes the binding's buffer allocations (torch caching allocator)"}
+    return {"ms_per_step": round(ms, 4), "tflops_dense_equiv": round(dense / (ms * 1e-3) / 1e12, 3)}
 
 
 def sweep_point(args, alpha, c):
@@ -370,7 +514,9 @@ def sweep_point(args, alpha, c):
            "tflops_executed": round(sum(w["flops"].values()) / (msv * 1e-3) / 1e12, 3),
            "block_density": round(w["block_density"], 4),
            "zero_fraction_sampled": round(r.zero_fraction(), 5),
-           "solver_passes_mean": round(w["passes_mean"], 3)}
+           "solver_passes_mean": round(w["passes_mean"], 3),
+           "solver_evals_mean": round(w["evals_mean"], 3),
+           "sum_p_minus_1_max_sampled": r.sum_p_error()}
     del r
     torch.cuda.empty_cache()
     return out
@@ -394,10 +540,13 @@ def other_configs(args, steps=5):
         ms, _, _ = r.timed(steps, 2, per_kernel=False)
         w = r.work()
         flops = (14.0 if bwd else 4.0) * n * n * d * B * H * (0.5 if causal else 1.0)
+        executed = sum(v_ for k_, v_ in w["flops"].items()
+                       if bwd or k_ in ("tau_solve", "fwd_sparse"))
         out.append({"config": name, "shape": "B%d H%d n%d d%d %s%s" % (
                         B, H, n, d, dt, " causal" if causal else ""),
                     "c": c, "fwd_bwd" if bwd else "fwd": True, "ms": round(ms, 4),
                     "tflops_dense_equiv": round(flops / (ms * 1e-3) / 1e12, 3),
+                    "tflops_executed": round(executed / (ms * 1e-3) / 1e12, 3),
                     "block_density": round(w["block_density"], 4),
                     "solver_passes_mean": round(w["passes_mean"], 3)})
         del r
@@ -461,6 +610,26 @@ def cpu_baseline(runner, heads):
 
 def main():
     args = parse()
+    if args.kernel_stats_from:
+        stats_csv, bench_json, out_md = args.kernel_stats_from
+        line = json.loads(open(bench_json).read().strip().splitlines()[-1])
+        base = ("python bench.py --steps %d --warmup %d --sweep= --long= --no-configs "
+                "--no-cpu-baseline --no-rows" % (line["steps"], line["warmup"]))
+        write_kernel_stats(stats_csv, bench_json, out_md,
+                           "%s > %s\nrocprofv3 --kernel-trace --stats --output-format csv -d %s -o run "
+                           "-- %s\npython bench.py --kernel-stats-from %s %s %s"
+                           % (base, bench_json, os.path.dirname(stats_csv), base, stats_csv,
+                              bench_json, out_md))
+        return
+    if args.mfma_from:
+        run = ("-- python bench.py --steps 2 --warmup 1 --sweep= --long= --no-configs "
+               "--no-cpu-baseline --no-rows")
+        write_mfma(args.mfma_from,
+                   "rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_BF16 --output-format csv -d %s "
+                   "-o run %s\npython bench.py --mfma-from %s"
+                   % (os.path.dirname(args.mfma_from), run, args.mfma_from),
+                   head_dim=args.head_dim)
+        return
     if args.traffic_from:
         mib = args.calib_copy_mib or 1024
         fetch_csv, write_csv = args.traffic_from
@@ -494,6 +663,14 @@ def main():
         t = kern[name]
         kernels[name] = {"ms": round(t, 4),
                          "tflops": round(work["flops"][name] / (t * 1e-3) / 1e12, 2) if t > 0 else 0.0}
+        if name in PROFILE_NAMES:
+            mf = measured_mfma(name)
+            tr = measured_traffic(name)
+            # from the committed counter summaries (null once the sources changed)
+            kernels[name]["mfma_busy"] = round(mf[0], 4) if mf else None
+            kernels[name]["mfma_executed_tflops"] = (round(mf[1] / (t * 1e-3) / 1e12, 2)
+                                                     if mf and t > 0 else None)
+            kernels[name]["hbm_GBps"] = round(tr / (t * 1e-3) / 1e9, 1) if tr and t > 0 else None
     dom = max(("tau_solve", "fwd_sparse", "bwd_dkdv", "bwd_dq"), key=lambda k_: kern[k_])
     ach = work["flops"][dom] / (kern[dom] * 1e-3) / 1e12
     traffic = measured_traffic(dom)
@@ -501,7 +678,10 @@ def main():
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
                 "traffic": round(traffic) if traffic is not None else None,
                 "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, "
-                                "copy-calibrated)"}
+                                "copy-calibrated)",
+                "timing": "HIP events around the kernel's stage launch on the current stream, "
+                          "mean over the timed steps (no profiler attached)",
+                "mfma_busy": kernels[dom].get("mfma_busy")}
     if args.calib_copy_mib > 0:
         src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -524,11 +704,15 @@ def main():
         "executed_tflops": round(executed / (ms * 1e-3) / 1e12, 3),
         "executed_frac_of_peak": round(executed / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "wall_s_timed": round(wall, 4),
+        "step_ms": kern["_steps"],
         "kernels": kernels,
         "sparsity": {"block_density": round(work["block_density"], 4),
                      "zero_fraction_sampled": round(run.zero_fraction(), 5),
                      "solver_passes_mean": round(work["passes_mean"], 3),
-                     "solver_passes_max": work["passes_max"]},
+                     "solver_passes_max": work["passes_max"],
+                     "solver_evals_mean": round(work["evals_mean"], 3),
+                     "solver_evals_max": work["evals_max"],
+                     "sum_p_minus_1_max_sampled": run.sum_p_error()},
         "roofline": roofline,
     }
     vals = lambda text: [float(x) for x in text.split(",") if x.strip()]

@@ -71,8 +71,10 @@ typedef struct {
  *   q_index    i32   [BH, T, T]    row (b,h,i): Q_i ascending in its first q_count entries
  *   k_count    i32   [BH, T]       |K_j|, query blocks listed for key block j
  *   k_index    i32   [BH, T, T]    row (b,h,j): K_j ascending in its first k_count entries
- *   stats      i32   [BH, T]       optional (may be NULL): K passes the solver ran for each
- *                                  64-row query block (1 max pass + evaluation passes)
+ *   stats      i32   [2, BH, T]    optional (may be NULL), per 64-row query block: [0] the K
+ *                                  passes the solver streamed (1 max pass + evaluations that
+ *                                  did not run on cached scores), [1] its evaluations of
+ *                                  f, f', f'' (Algorithm 1 iterations, Eq. 3-7)
  *   tau_lo     fp32  [BH, n]       fp32 inputs only (required then; ignored, may be NULL,
  *                                  for bf16): the threshold is tau + tau_lo to ~fp64
  *                                  precision.  For alpha not in {1.25, 1.5, 2} the fp32

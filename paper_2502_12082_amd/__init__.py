@@ -208,7 +208,8 @@ class Residuals:
         self.q_index = torch.empty(BH * T * T, dtype=torch.int32, device=device).view(BH, T, T)
         self.k_count = torch.empty(BH * T, dtype=torch.int32, device=device).view(BH, T)
         self.k_index = torch.empty(BH * T * T, dtype=torch.int32, device=device).view(BH, T, T)
-        self.stats = (torch.empty(z.stats // 4, dtype=torch.int32, device=device)
+        # [0]: K passes the solver streamed, [1]: its evaluations, per query block
+        self.stats = (torch.empty(z.stats // 4, dtype=torch.int32, device=device).view(2, BH, T)
                       if with_stats else None)
         # fp32 inputs: the low part of tau (tau + tau_lo to ~fp64 precision)
         self.tau_lo = (torch.empty(z.tau_lo // 4, dtype=torch.float32, device=device).view(BH, n)
@@ -288,7 +289,7 @@ def _check_residuals(res, shape: Shape, device, need_o2: bool):
     _need(res.k_count, "res.k_count", (BH, T), torch.int32, device)
     _need(res.k_index, "res.k_index", (BH, T, T), torch.int32, device)
     if res.stats is not None:
-        _need(res.stats, "res.stats", (res.sizes.stats // 4,), torch.int32, device)
+        _need(res.stats, "res.stats", (2, BH, T), torch.int32, device)
     if shape.dtype == EA_F32:
         _need(res.tau_lo, "res.tau_lo", (BH, n), torch.float32, device)
 

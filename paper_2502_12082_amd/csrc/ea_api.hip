@@ -97,7 +97,7 @@ void fill_sizes(const Dims& d, ea_sizes* z) {
   z->q_index = (size_t)(d.BH * d.T * d.T) * 4;
   z->k_count = z->q_count;
   z->k_index = z->q_index;
-  z->stats = (size_t)(d.BH * d.T) * 4;
+  z->stats = (size_t)(2 * d.BH * d.T) * 4;
   z->ws_fwd = (size_t)solve_slots(d) * SOLVE_SLOT_BYTES;
   z->ws_bwd = bwd_ws_bytes(d);
   z->tau_lo = d.dtype == EA_F32 ? (size_t)(d.BH * d.n) * 4 : 0;

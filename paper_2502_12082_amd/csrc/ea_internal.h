@@ -36,7 +36,7 @@ struct TauArgs {
   const void* k;
   float* tau;         // [BH, n]
   uint8_t* mask;      // [BH, T, T]
-  int32_t* stats;     // [BH, T] K passes run for each 64-row query block, or null
+  int32_t* stats;     // [2, BH, T] K passes and evaluations for each 64-row query block, or null
   // no-mask mode only (mask, stats null): O and, when training, O2 are
   // accumulated by the solver kernel itself once tau is known
   const void* v;

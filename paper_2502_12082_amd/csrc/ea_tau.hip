@@ -991,6 +991,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   }
 
   int passes = 1;  // K passes (streamed), the max pass included
+  int evals = 0;   // evaluations of f, f', f'' (Algorithm 1 iterations)
   // Evaluations run on the lists when every one of them fit.  Entries below
   // the final bound (collected while it was still rising) stay: at any tau
   // of the bracket their z is clamped to exactly 0, as in a streamed pass.
@@ -1179,6 +1180,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     // end from the returned tau, so the update from this last evaluation
     // is still taken: one more Halley step costs nothing there.
     const bool stop = __syncthreads_and(conv) || it >= a.max_iter;
+    evals = it + 1;
     if (stop && !cached) break;
 #pragma unroll
     for (int gq = 0; gq < 2; ++gq) {
@@ -1316,7 +1318,10 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     const uint8_t b = (bits[w * BW + (kb >> 5)] >> (kb & 31)) & 1u;
     a.mask[((size_t)bh * T + qb) * T + kb] = b;
   }
-  if (a.stats && lane == 0) a.stats[(size_t)bh * T + qb] = passes;
+  if (a.stats && lane == 0) {
+    a.stats[(size_t)bh * T + qb] = passes;
+    a.stats[((size_t)a.BH + bh) * T + qb] = evals;
+  }
 }
 
 template <typename E, int D, int MODE>

@@ -53,7 +53,7 @@ def test_sizes():
     assert z.block_mask == BH * T * T
     assert z.q_count == z.k_count == BH * T * 4
     assert z.q_index == z.k_index == BH * T * T * 4
-    assert z.stats == BH * T * 4
+    assert z.stats == 2 * BH * T * 4
     # solver cache: one slot per 256-row tile, each 2 lists x 192 entries x
     # 256 threads x 8 bytes
     assert z.ws_fwd == BH * ((n + 255) // 256) * (2 * 192 * 256 * 8) and z.ws_bwd == BH * n * 4

@@ -64,3 +64,25 @@ def test_traffic_summary_round_trip(tmp_path, monkeypatch):
     (tmp_path / "traffic_tau_solve.md").write_text(
         text.replace(bench.sources_sha256("tau_solve"), "0" * 64))
     assert bench.measured_traffic("tau_solve") is None
+
+
+def test_mfma_summary_round_trip(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "mfma_path", lambda k: str(tmp_path / ("mfma_%s.md" % k)))
+    dkdv = "void ea::(anonymous namespace)::dkdv2_kernel<128, 2>(ea::BwdArgs)"
+    dkdv64 = "void ea::(anonymous namespace)::dkdv2_kernel<64, 2>(ea::BwdArgs)"
+    pmc = tmp_path / "pmc.csv"
+    with open(pmc, "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=["Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for name, util, mops in ((dkdv, 40.0, 1000), (dkdv, 42.0, 1000), (dkdv64, 90.0, 5)):
+            w.writerow({"Kernel_Name": name, "Counter_Name": "MfmaUtil", "Counter_Value": util})
+            w.writerow({"Kernel_Name": name, "Counter_Name": "SQ_INSTS_VALU_MFMA_MOPS_BF16",
+                        "Counter_Value": mops})
+    bench.write_mfma(str(pmc), "cmd", head_dim=128)
+    busy, flops = bench.measured_mfma("bwd_dkdv")
+    assert abs(busy - 0.41) < 1e-9 and flops == 1000 * 512
+    assert bench.measured_mfma("bwd_dq") is None
+    text = (tmp_path / "mfma_bwd_dkdv.md").read_text()
+    (tmp_path / "mfma_bwd_dkdv.md").write_text(
+        text.replace(bench.sources_sha256("bwd_dkdv"), "0" * 64))
+    assert bench.measured_mfma("bwd_dkdv") is None

@@ -53,12 +53,12 @@ def test_cache_matches_streaming(alpha, causal, c):
     t0, t1 = r0.tau.double(), r1.tau.double()
     dt = ((t1 - t0).abs() / t0.abs().clamp(min=1.0)).max().item()
     do = (o1.float() - o0.float()).abs().max().item()
-    log("  dtau %.2e  dO %.2e  K passes %s -> %s" % (dt, do, r0.stats.float().mean().item(),
-                                                      r1.stats.float().mean().item()))
+    log("  dtau %.2e  dO %.2e  K passes %s -> %s" % (dt, do, r0.stats[0].float().mean().item(),
+                                                      r1.stats[0].float().mean().item()))
     assert dt <= 1e-4
     assert do <= BF16_TOL
     # the cache adds at most one K pass per fill attempt (two attempts)
-    assert (r1.stats <= r0.stats + 2).all()
+    assert (r1.stats[0] <= r0.stats[0] + 2).all()
 
 
 @pytest.mark.parametrize("alpha", [1.5, 3.0])
@@ -88,7 +88,7 @@ def test_cache_engages_at_high_sparsity():
     pass (a tile whose lists overflow streams K instead)."""
     inp = synth.attention_inputs(1, 4, 4096, 128, c=1.0, dtype="bf16", seed=5)
     (o0, r0), (o1, r1) = _both(inp, 1.5, False)
-    p0, p1 = r0.stats.float().mean().item(), r1.stats.float().mean().item()
+    p0, p1 = r0.stats[0].float().mean().item(), r1.stats[0].float().mean().item()
     log("K passes: streaming %.2f, cached %.2f" % (p0, p1))
     assert p1 <= p0 - 1.0
     assert p1 <= 2.2
@@ -115,7 +115,7 @@ def test_cache_retry_after_overflow():
     streaming either way."""
     inp = synth.attention_inputs(1, 2, 8192, 128, c=2.0, dtype="bf16", seed=synth.SEED_BASE)
     (o0, r0), (o1, r1) = _both(inp, 1.25, False)
-    s0, s1 = r0.stats, r1.stats
+    s0, s1 = r0.stats[0], r1.stats[0]
     dt = ((r1.tau.double() - r0.tau.double()).abs() / r0.tau.double().abs().clamp(min=1.0))
     do = (o1.float() - o0.float()).abs().max().item()
     retried = ((s1 > 1) & (s1 < s0)).float().mean().item()

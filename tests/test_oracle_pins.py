@@ -108,7 +108,8 @@ def test_brute_force_supports(alpha):
 
 
 def test_golden_examples():
-    files = sorted(glob.glob(os.path.join(HERE, "golden", "*.json")))
+    files = sorted(f for f in glob.glob(os.path.join(HERE, "golden", "*.json"))
+                   if not os.path.basename(f).startswith("alg1_"))
     assert len(files) >= 6
     for fn in files:
         e = json.load(open(fn))
@@ -153,6 +154,17 @@ def test_special_cases(alpha):
     x = np.array([3.0, 1.5, 0.0, -2.0])  # gap >= 1: one-hot, tau = max - 1
     p, tau = oracle.entmax(x, alpha)
     assert abs(tau - 2.0) < 1e-12 and np.array_equal(p, [1.0, 0, 0, 0])
+
+
+@pytest.mark.parametrize("name", ["alg1_trace_a15", "alg1_trace_a125"])
+def test_halley_bisection_trace_iterates(name):
+    """The oracle's fp64 Algorithm 1 iterates against the exact rational ones
+    (tests/golden/make_golden.py; the first update is derived by hand there:
+    19/106 at alpha 1.5, where a Newton step would give 7/40, and
+    4871/64004 at alpha 1.25, which a wrong f'' coefficient would miss)."""
+    ex = json.load(open(os.path.join(HERE, "golden", name + ".json")))
+    tr = oracle.halley_bisection_trace(np.array(ex["x"]), ex["alpha"], ex["iters"])
+    assert np.allclose(tr, ex["tau"], rtol=1e-14, atol=1e-15), (tr, ex["tau"])
 
 
 def test_halley_bisection_trace_converges():
