@@ -144,10 +144,22 @@ def test_long_context(n):
     n = 16384 also on a key block in the middle (rows from there on)."""
     T = n // 64
     col_blocks = [T // 2, T - 1] if n <= 16384 else None
-    gpu, _ = _sampled_case(1, 8, n, 64, 1.5, True, 16.0, block_rows=[0, T // 2, T - 1],
-                           ncols=64, heads=[0, 7], label="long", col_blocks=col_blocks)
+    gpu, inp = _sampled_case(1, 8, n, 64, 1.5, True, 16.0, block_rows=[0, T // 2, T - 1],
+                             ncols=64, heads=[0, 7], label="long", col_blocks=col_blocks)
     check_tables({k: gpu[k][:1] for k in ("mask", "q_count", "q_index", "k_count", "k_index")},
                  True)
+    # tau on 48 random rows of every head, and O on those rows of heads 0 and 7
+    rng = np.random.default_rng(n)
+    for bh in range(8):
+        rows = np.sort(rng.choice(n, size=48, replace=False))
+        ref = oracle_head(inp, bh, 1.5, 64 ** -0.5, True, False, rows=rows)
+        tr, tg = ref["tau"][rows], gpu["tau"][bh][rows]
+        rel = np.max(np.abs(tg - tr) / np.maximum(1.0, np.abs(tr)))
+        assert rel <= 1e-3, ("long random rows", bh, rel)
+        if bh in (0, 7):
+            err = np.max(np.abs(gpu["o"][bh][rows] - ref["o"][rows]))
+            assert err <= 2e-2, ("long random rows O", bh, err)
+    log("  random rows: tau and O within bounds on all heads")
 
 
 # ------------------------------------------------------------- invariants
