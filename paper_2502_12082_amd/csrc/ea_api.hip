@@ -82,11 +82,18 @@ ea_status check_shape(const ea_shape* s, const ea_params* p, Dims* out) {
 // delta, one fp32 per row
 size_t bwd_ws_bytes(const Dims& d) { return (size_t)(d.BH * d.n) * 4; }
 
-// One cache slot per solver workgroup: 256-row tiles for the masked path,
-// 128-row tiles for the no-mask fused forward.  The masked path's sizing
-// covers both.
-int64_t solve_slots(const Dims& d) { return d.BH * ((d.n + SOLVE_ROWS - 1) / SOLVE_ROWS); }
-int64_t cache_slots(const Dims& d) { return d.BH * ((d.n + TAU_ROWS - 1) / TAU_ROWS); }
+// One cache slot per solver tile (256 rows on the masked path, 128 rows in
+// the no-mask fused forward), at most MAX_SOLVE_SLOTS of the masked path's
+// size: two co-resident workgroups per CU of a 256-CU MI355X.  With fewer
+// slots than tiles the solvers run one workgroup per slot, each solving
+// tiles in turn, so the workspace does not grow with B * H * n.  The masked
+// path's sizing covers both.
+constexpr int64_t MAX_SOLVE_SLOTS = 512;
+int64_t solve_tiles(const Dims& d) { return d.BH * ((d.n + SOLVE_ROWS - 1) / SOLVE_ROWS); }
+int64_t cache_tiles(const Dims& d) { return d.BH * ((d.n + TAU_ROWS - 1) / TAU_ROWS); }
+int64_t solve_slots(const Dims& d) {
+  return solve_tiles(d) < MAX_SOLVE_SLOTS ? solve_tiles(d) : MAX_SOLVE_SLOTS;
+}
 static_assert(SOLVE_ROWS == 2 * TAU_ROWS, "a masked-path slot covers two fused-forward slots");
 
 void fill_sizes(const Dims& d, ea_sizes* z) {
@@ -237,11 +244,11 @@ ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const
     // The cache is optional: tiles without a slot (all of them when there is
     // no workspace) stream K on every solver pass.
     int64_t slots = workspace ? (int64_t)(ws_bytes / SOLVE_SLOT_BYTES) : 0;
-    const int64_t most = solve_slots(d);
+    const int64_t most = solve_tiles(d);
     if (slots > most) slots = most;
     CandEntry* cand = slots > 0 ? static_cast<CandEntry*>(workspace) : nullptr;
     TauArgs ta{q, k, res->tau, res->block_mask, res->stats, nullptr, nullptr, nullptr, cand,
-               TAU_CACHE_CAP, (int)slots,
+               TAU_CACHE_CAP, (int)slots, /*tile0=*/0,
                (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma, params->causal,
                params->max_iter, params->tol, gk,
                const_cast<float*>(tau_lo_of(res, d)), c64_of(params), g64_of(params)};
@@ -407,12 +414,13 @@ ea_status entmax_attn_fwd_dense(const ea_shape* shape, const ea_params* params, 
   if (params->need_bwd && !tensor_ok(o2)) return EA_ERR_INVALID_ARG;
   if (workspace && !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
   int64_t slots = workspace ? (int64_t)(ws_bytes / TAU_SLOT_BYTES) : 0;
-  if (slots > cache_slots(d)) slots = cache_slots(d);
+  if (slots > cache_tiles(d)) slots = cache_tiles(d);
   CandEntry* cand = slots > 0 ? static_cast<CandEntry*>(workspace) : nullptr;
   const float c = (params->alpha - 1.0f) * params->scale;
   const float gamma = 1.0f / (params->alpha - 1.0f);
   TauArgs ta{q, k, tau, nullptr, nullptr, v, o, params->need_bwd ? o2 : nullptr, cand,
-             TAU_CACHE_CAP, (int)slots, (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma,
+             TAU_CACHE_CAP, (int)slots, /*tile0=*/0, (int)d.BH, (int)d.n, (int)d.T, c,
+             params->alpha, gamma,
              params->causal, params->max_iter, params->tol, gamma_kind(params->alpha), nullptr,
              c64_of(params), g64_of(params)};
   return from_hip(launch_tau_fused(ta, d.dtype, (int)d.d, static_cast<hipStream_t>(stream)));

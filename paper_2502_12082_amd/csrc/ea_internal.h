@@ -44,7 +44,8 @@ struct TauArgs {
   float* o2;          // [BH, n, D] fp32, or null (inference)
   CandEntry* cand;    // candidate cache: one slot of 2 * rows * cap entries per workgroup, or null
   int cap;            // entries per list
-  int slots;          // workgroups with a cache slot (workgroup t uses slot t)
+  int slots;          // cache slots (workgroup b of a launch uses slot b)
+  int tile0;          // first tile of this launch (workgroup b solves tile tile0 + b)
   int BH, n, T;
   float c;            // (alpha - 1) * scale
   float alpha, gamma;

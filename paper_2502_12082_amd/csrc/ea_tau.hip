@@ -64,11 +64,13 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
   // The Newton step from any tau is a lower bound of the root when f is
   // convex, i.e. gamma >= 1 (alpha <= 2).
   const bool newton_bound = g >= 1.f;
-  // This workgroup's slot of the candidate cache (entry e of thread t at
-  // [e * TAU_NT + t]), or null when the workspace has no slot for it.
-  const int tile = blockIdx.x;
+  // Tile a.tile0 + blockIdx.x, and this workgroup's slot of the candidate
+  // cache (entry e of thread t at [e * TAU_NT + t]), or null when the
+  // workspace has no slot for it.  A launch covers at most one tile per slot
+  // (see launch_tiles).
+  const int tile = a.tile0 + (int)blockIdx.x;
   CandEntry* const cache =
-      a.cand && tile < a.slots ? a.cand + (size_t)tile * a.cap * TAU_NT : nullptr;
+      a.cand && (int)blockIdx.x < a.slots ? a.cand + (size_t)blockIdx.x * a.cap * TAU_NT : nullptr;
 
   TileDma<TL, D, TAU_NT> dma;
   dma.init();
@@ -573,7 +575,13 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   const int TW = (T + 31) / 32;
   const float c = a.c, g = a.gamma;
   const bool newton_bound = g >= 1.f;  // f convex: Newton steps bound the root from below
-  const int tile = blockIdx.x;
+  // Tile a.tile0 + blockIdx.x, and this workgroup's cache slot: list (thread
+  // t, group gq) holds entry e at [(2 e + gq) * SV_NT + t]; null without a
+  // slot.  A launch covers at most one tile per slot (see launch_tiles).
+  const int tile = a.tile0 + (int)blockIdx.x;
+  CandEntry* const cache = a.cand && (int)blockIdx.x < a.slots
+                               ? a.cand + (size_t)blockIdx.x * a.cap * 2 * SV_NT
+                               : nullptr;
   const int bh = tile % a.BH;
   int qt = tile / a.BH;
   if (a.causal) qt = nqt - 1 - qt;  // longest rows first
@@ -592,10 +600,6 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   const E* K = static_cast<const E*>(a.k) + (size_t)bh * n * D;
   const int wg_last = min(n, (qt + 1) * SV_ROWS) - 1;
   const int nkb = a.causal ? wg_last / BLK + 1 : T;
-  // this workgroup's cache slot: list (thread t, group gq) holds entry e at
-  // [(2 e + gq) * SV_NT + t]; null without a slot
-  CandEntry* const cache =
-      a.cand && tile < a.slots ? a.cand + (size_t)tile * a.cap * 2 * SV_NT : nullptr;
 
   TileDma<TL, D, SV_NT> dma;
   dma.init();
@@ -1324,24 +1328,40 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   }
 }
 
+// One workgroup per tile.  With a workspace of fewer slots than tiles the
+// tiles go in launches of at most `slots` workgroups, each workgroup using
+// the slot of its index, so that no two workgroups in flight share a slot
+// (launches on one stream run in order).  Causal tiles come longest first,
+// so each launch holds tiles of similar length.
+template <typename K>
+hipError_t launch_tiles(K kernel, TauArgs a, int rows, int threads, hipStream_t s) {
+  const int tiles = a.BH * ((a.n + rows - 1) / rows);
+  const int per = a.cand && a.slots > 0 && a.slots < tiles ? a.slots : tiles;
+  for (int t0 = 0; t0 < tiles; t0 += per) {
+    a.tile0 = t0;
+    const hipError_t e = launch_kernel(kernel, dim3((unsigned)(tiles - t0 < per ? tiles - t0 : per)),
+                                       dim3(threads), s, a);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 template <typename E, int D, int MODE>
 hipError_t launch_tau_d(const TauArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)(a.BH * ((a.n + TAU_ROWS - 1) / TAU_ROWS))), block(TAU_NT);
   auto kernel = tau_solve_kernel<E, D, 0, MODE>;
   if (a.gk == 1) kernel = tau_solve_kernel<E, D, 1, MODE>;
   if (a.gk == 2) kernel = tau_solve_kernel<E, D, 2, MODE>;
   if (a.gk == 4) kernel = tau_solve_kernel<E, D, 4, MODE>;
-  return launch_kernel(kernel, grid, block, s, a);
+  return launch_tiles(kernel, a, TAU_ROWS, TAU_NT, s);
 }
 
 template <typename E, int D>
 hipError_t launch_solve_d(const TauArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)(a.BH * ((a.n + SV_ROWS - 1) / SV_ROWS))), block(SV_NT);
   auto kernel = solve_kernel<E, D, 0>;
   if (a.gk == 1) kernel = solve_kernel<E, D, 1>;
   if (a.gk == 2) kernel = solve_kernel<E, D, 2>;
   if (a.gk == 4) kernel = solve_kernel<E, D, 4>;
-  return launch_kernel(kernel, grid, block, s, a);
+  return launch_tiles(kernel, a, SV_ROWS, SV_NT, s);
 }
 
 template <int MODE>
