@@ -482,10 +482,10 @@ def dense_mode_bench(run, steps=5, warmup=2):
     def step():
         ea._check(ea._lib.entmax_attn_fwd_dense(
             ctypes.byref(shape), ctypes.byref(p), ptr(q), ptr(k), ptr(v), ptr(o), ptr(tau),
-            ptr(o2), ptr(ws), ws.numel(), stream), "entmax_attn_fwd_dense")
+            None, ptr(o2), ptr(ws), ws.numel(), stream), "entmax_attn_fwd_dense")
         ea._check(ea._lib.entmax_attn_bwd_dense(
             ctypes.byref(shape), ctypes.byref(p), ptr(q), ptr(k), ptr(v), ptr(do), ptr(tau),
-            ptr(o2), ptr(dq), ptr(dk), ptr(dv), ptr(wsb), wsb.numel() * 4, stream),
+            None, ptr(o2), ptr(dq), ptr(dk), ptr(dv), ptr(wsb), wsb.numel() * 4, stream),
             "entmax_attn_bwd_dense")
 
     for _ in range(warmup):

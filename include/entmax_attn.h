@@ -196,6 +196,9 @@ ea_status entmax_attn_bwd_noalloc(const ea_shape* shape, const ea_params* params
  * per 128-row query tile, visiting every valid key block; no block mask or
  * tables exist, so memory beyond the inputs and outputs is O(n) per head.
  *   tau  fp32 [BH, n] (written); o2 fp32 [BH, n, d] (written if need_bwd)
+ *   tau_lo  fp32 [BH, n], fp32 inputs only (required then, written by the
+ *        forward and read by the backward; ignored, may be NULL, for bf16):
+ *        the low part of the threshold, as ea_residuals.tau_lo
  *   workspace  optional candidate cache, as for entmax_attn_fwd
  * The backward visits every valid block (no tables) and otherwise follows
  * entmax_attn_bwd: workspace >= sizes.ws_bwd bytes.  Results equal those of
@@ -203,12 +206,12 @@ ea_status entmax_attn_bwd_noalloc(const ea_shape* shape, const ea_params* params
  * (forward) or three (backward) on `stream`.
  */
 ea_status entmax_attn_fwd_dense(const ea_shape* shape, const ea_params* params, const void* q,
-                                const void* k, const void* v, void* o, float* tau, float* o2,
-                                void* workspace, size_t ws_bytes, void* stream);
+                                const void* k, const void* v, void* o, float* tau, float* tau_lo,
+                                float* o2, void* workspace, size_t ws_bytes, void* stream);
 ea_status entmax_attn_bwd_dense(const ea_shape* shape, const ea_params* params, const void* q,
                                 const void* k, const void* v, const void* dout, const float* tau,
-                                const float* o2, float* dq, float* dk, float* dv, void* workspace,
-                                size_t ws_bytes, void* stream);
+                                const float* tau_lo, const float* o2, float* dq, float* dk,
+                                float* dv, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Row-wise alpha-entmax of a materialized score matrix s, [rows, n] row-major

@@ -83,11 +83,11 @@ _lib.entmax_attn_bwd_stage.argtypes = [ctypes.c_int, _P(Shape), _P(Params), _v, 
 _lib.entmax_attn_bwd_stage.restype = ctypes.c_int
 _lib.entmax_attn_status_string.argtypes = [ctypes.c_int]
 _lib.entmax_attn_status_string.restype = ctypes.c_char_p
-_lib.entmax_attn_fwd_dense.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _v, _v, _v,
+_lib.entmax_attn_fwd_dense.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _v, _v, _v, _v,
                                        ctypes.c_size_t, _v]
 _lib.entmax_attn_fwd_dense.restype = ctypes.c_int
 _lib.entmax_attn_bwd_dense.argtypes = [_P(Shape), _P(Params), _v, _v, _v, _v, _v, _v, _v, _v, _v,
-                                       _v, ctypes.c_size_t, _v]
+                                       _v, _v, ctypes.c_size_t, _v]
 _lib.entmax_attn_bwd_dense.restype = ctypes.c_int
 _lib.entmax_rows_fwd.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int, _P(Params), _v, _v,
                                  _v, _v]
@@ -423,7 +423,9 @@ def rows_backward(s, tau, dp, alpha=1.5, scale=1.0):
 
 def forward_dense(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, max_iter=None,
                   tol=None, workspace=None):
-    """(O, tau, O2 or None) without block mask or tables (Algorithm 2 as written)."""
+    """(O, tau, O2 or None, tau_lo or None) without block mask or tables
+    (Algorithm 2 as written); tau_lo, the threshold's low part, exists for fp32
+    inputs and goes back into backward_dense."""
     shape = make_shape(q)
     dev = _check_qkv([("q", q), ("k", k), ("v", v)], shape)
     _on_gpu(dev)
@@ -431,6 +433,7 @@ def forward_dense(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, m
     B, H, n, d = q.shape
     o = torch.empty_like(q)
     tau = torch.empty((B * H, n), dtype=torch.float32, device=q.device)
+    tau_lo = torch.empty_like(tau) if q.dtype == torch.float32 else None
     o2 = torch.empty(q.shape, dtype=torch.float32, device=q.device) if need_bwd else None
     z = entmax_attn_sizes(shape, params)
     if workspace is None:
@@ -442,18 +445,24 @@ def forward_dense(q, k, v, alpha=1.5, scale=None, causal=False, need_bwd=True, m
                                                             workspace.numel() * workspace.element_size())
     _check(_lib.entmax_attn_fwd_dense(ctypes.byref(shape), ctypes.byref(params), q.data_ptr(),
                                       k.data_ptr(), v.data_ptr(), o.data_ptr(), tau.data_ptr(),
+                                      tau_lo.data_ptr() if tau_lo is not None else None,
                                       o2.data_ptr() if o2 is not None else None, ws_ptr, ws_bytes,
                                       _stream_handle(q.device)), "entmax_attn_fwd_dense")
-    return o, tau, o2
+    return o, tau, o2, tau_lo
 
 
-def backward_dense(q, k, v, dout, tau, o2, alpha=1.5, scale=None, causal=False):
-    """(dQ, dK, dV) in fp32 for the no-mask forward that produced tau and o2."""
+def backward_dense(q, k, v, dout, tau, o2, alpha=1.5, scale=None, causal=False, tau_lo=None):
+    """(dQ, dK, dV) in fp32 for the no-mask forward that produced tau, o2 and
+    (fp32 inputs) tau_lo."""
     shape = make_shape(q)
     dev = _check_qkv([("q", q), ("k", k), ("v", v), ("dout", dout)], shape)
     B, H, n, d = q.shape
     _need(tau, "tau", (B * H, n), torch.float32, dev)
     _need(o2, "o2", q.shape, torch.float32, dev)
+    if q.dtype == torch.float32:
+        if tau_lo is None:
+            raise ValueError("backward_dense: fp32 inputs need the forward's tau_lo")
+        _need(tau_lo, "tau_lo", (B * H, n), torch.float32, dev)
     _on_gpu(dev)
     params = make_params(alpha, scale, causal, True, None, None, head_dim=q.shape[-1])
     z = entmax_attn_sizes(shape, params)
@@ -462,6 +471,7 @@ def backward_dense(q, k, v, dout, tau, o2, alpha=1.5, scale=None, causal=False):
     ws = torch.empty(max(z.ws_bwd, 16) // 4 + 4, dtype=torch.float32, device=q.device)
     _check(_lib.entmax_attn_bwd_dense(ctypes.byref(shape), ctypes.byref(params), q.data_ptr(),
                                       k.data_ptr(), v.data_ptr(), dout.data_ptr(), tau.data_ptr(),
+                                      tau_lo.data_ptr() if q.dtype == torch.float32 else None,
                                       o2.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
                                       ws.data_ptr(), ws.numel() * 4, _stream_handle(q.device)),
            "entmax_attn_bwd_dense")

@@ -404,13 +404,14 @@ ea_status entmax_rows_bwd(int64_t rows, int32_t n, ea_dtype dtype, const ea_para
 }
 
 ea_status entmax_attn_fwd_dense(const ea_shape* shape, const ea_params* params, const void* q,
-                                const void* k, const void* v, void* o, float* tau, float* o2,
-                                void* workspace, size_t ws_bytes, void* stream) {
+                                const void* k, const void* v, void* o, float* tau, float* tau_lo,
+                                float* o2, void* workspace, size_t ws_bytes, void* stream) {
   Dims d;
   ea_status st = check_shape(shape, params, &d);
   if (st != EA_OK) return st;
   if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(o)) return EA_ERR_INVALID_ARG;
   if (!small_ok(tau)) return EA_ERR_INVALID_ARG;
+  if (d.dtype == EA_F32 && !small_ok(tau_lo)) return EA_ERR_INVALID_ARG;
   if (params->need_bwd && !tensor_ok(o2)) return EA_ERR_INVALID_ARG;
   if (workspace && !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
   int64_t slots = workspace ? (int64_t)(ws_bytes / TAU_SLOT_BYTES) : 0;
@@ -421,26 +422,28 @@ ea_status entmax_attn_fwd_dense(const ea_shape* shape, const ea_params* params, 
   TauArgs ta{q, k, tau, nullptr, nullptr, v, o, params->need_bwd ? o2 : nullptr, cand,
              TAU_CACHE_CAP, (int)slots, /*tile0=*/0, (int)d.BH, (int)d.n, (int)d.T, c,
              params->alpha, gamma,
-             params->causal, params->max_iter, params->tol, gamma_kind(params->alpha), nullptr,
-             c64_of(params), g64_of(params)};
+             params->causal, params->max_iter, params->tol, gamma_kind(params->alpha),
+             d.dtype == EA_F32 ? tau_lo : nullptr, c64_of(params), g64_of(params)};
   return from_hip(launch_tau_fused(ta, d.dtype, (int)d.d, static_cast<hipStream_t>(stream)));
 }
 
 ea_status entmax_attn_bwd_dense(const ea_shape* shape, const ea_params* params, const void* q,
                                 const void* k, const void* v, const void* dout, const float* tau,
-                                const float* o2, float* dq, float* dk, float* dv, void* workspace,
-                                size_t ws_bytes, void* stream) {
+                                const float* tau_lo, const float* o2, float* dq, float* dk,
+                                float* dv, void* workspace, size_t ws_bytes, void* stream) {
   Dims d;
   ea_status st = check_shape(shape, params, &d);
   if (st != EA_OK) return st;
   if (!tensor_ok(q) || !tensor_ok(k) || !tensor_ok(v) || !tensor_ok(dout)) return EA_ERR_INVALID_ARG;
   if (!tensor_ok(dq) || !tensor_ok(dk) || !tensor_ok(dv)) return EA_ERR_INVALID_ARG;
   if (!small_ok(tau) || !tensor_ok(o2)) return EA_ERR_INVALID_ARG;
+  if (d.dtype == EA_F32 && !small_ok(tau_lo)) return EA_ERR_INVALID_ARG;
   if (!workspace || !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
   if (ws_bytes < bwd_ws_bytes(d)) return EA_ERR_WORKSPACE;
   // no tables: the kernels visit every valid block
   ea_residuals res{};
   res.tau = const_cast<float*>(tau);
+  res.tau_lo = const_cast<float*>(tau_lo);
   res.o2 = const_cast<float*>(o2);
   hipStream_t s = static_cast<hipStream_t>(stream);
   for (int stage = 0; stage < 3; ++stage)

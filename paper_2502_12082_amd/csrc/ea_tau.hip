@@ -454,12 +454,66 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
       }
     }
 
-    if (row_ok && lane < 32) a.tau[(size_t)bh * n + i] = tau;
+    // fp32 inputs, general alpha (ea_common.h): tau refined in fp64 by Newton
+    // steps on f (Eq. 3, 6) over every entry above the lower edge of the band
+    // around the support edge, each with its fp64 score, as in solve_kernel.
+    constexpr bool PRECISE = precise_path<E, GK>();
+    double tau64 = tau;
+    [[maybe_unused]] const float band = PRECISE_BAND * fmaxf(1.f, fabsf(tau));
+    [[maybe_unused]] const float* Qf = reinterpret_cast<const float*>(Q);
+    [[maybe_unused]] const float* Kf = reinterpret_cast<const float*>(K);
+    if constexpr (PRECISE) {
+      // use(fp32 score, key) for every valid entry of this lane's row
+      auto visit = [&](auto&& use) {
+        if (cached) {
+          scan([&](const CandEntry& ce) { use(ce.s, ce.j); });
+        } else {
+          stream([&](int kb, const E* kt) {
+            const int j0 = kb * BLK;
+            const int k0 = sub_kind(j0), k1 = sub_kind(j0 + 32);
+            if (k0 == 0 && k1 == 0) return;
+            f32x16 s0, s1;
+            scores(kt, s0, s1);
+            if (k0 == 2) mask_tile(s0, j0);
+            if (k1 == 2) mask_tile(s1, j0 + 32);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              if (k0) use(s0[r], j0 + crow(r));
+              if (k1) use(s1[r], j0 + 32 + crow(r));
+            }
+          });
+        }
+      };
+      for (int it = 0; it < 3; ++it) {
+        double t0 = 0.0, t1 = 0.0;
+        visit([&](float sv, int jv) {
+          if (!row_ok || !(fmaf(c, sv, -tau) > -band)) return;
+          const double z = exact_x<D>(Qf + (size_t)i * D, Kf + (size_t)jv * D, a.c64) - tau64;
+          if (z > 0.0) {
+            t0 += pow(z, a.g64);
+            t1 += pow(z, a.g64 - 1.0);
+          }
+        });
+        t0 += __shfl_xor(t0, 32);
+        t1 += __shfl_xor(t1, 32);
+        if (row_ok && t1 > 0.0) {
+          const double slack = 1e-5 * fmax(1.0, fmax(fabs((double)lo), fabs((double)hi)));
+          const double tn = tau64 + (t0 - 1.0) / (a.g64 * t1);
+          tau64 = fmin(fmax(tn, (double)lo - slack), (double)hi + slack);
+        }
+      }
+    }
+    if (row_ok && lane < 32) {
+      const float th = (float)tau64;
+      a.tau[(size_t)bh * n + i] = th;
+      if (a.tau_lo) a.tau_lo[(size_t)bh * n + i] = PRECISE ? (float)(tau64 - (double)th) : 0.f;
+    }
 
     {
       // ---- Algorithm 2 at the returned tau: O = sum_j P_ij V_j, and in
       // training O2 = sum_j u_ij V_j / sum_j u_ij (sum u is the solver's last
-      // S1 sum), over every valid key block.
+      // S1 sum, or, on the fp64 path, the sum of the u this pass forms), over
+      // every valid key block.
       f32x16 o[NTD], o2[NTD];
 #pragma unroll
       for (int t = 0; t < NTD; ++t) {
@@ -469,15 +523,24 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
       const E* V = static_cast<const E*>(a.v) + (size_t)bh * n * D;
       TileDma<TV, D, TAU_NT> vdma;
       vdma.init();
-      auto pv_tile = [&](const f32x16& s, const E* vt, int sub) {
+      [[maybe_unused]] float usum_pv = 0.f;  // the fp64 path's sum of u
+      auto pv_tile = [&](const f32x16& s, const E* vt, int sub, int j0) {
         float p[16], u[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float zp = relu_z(c, s[r], tau);
-          if constexpr (TRAIN)
+          float zp;
+          if constexpr (PRECISE) {
+            zp = precise_relu_z<D>(row_ok, c, s[r], tau, band, tau64, Qf + (size_t)i * D,
+                                   Kf + (size_t)(j0 + 32 * sub + crow(r)) * D, a.c64);
+          } else {
+            zp = relu_z(c, s[r], tau);
+          }
+          if constexpr (TRAIN) {
             Gamma<GK>::pu(zp, g, p[r], u[r]);
-          else
+            if constexpr (PRECISE) usum_pv += u[r];
+          } else {
             p[r] = Gamma<GK>::p_only(zp, g);
+          }
         }
 #pragma unroll
         for (int t = 0; t < PS; ++t) {
@@ -512,9 +575,10 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
         scores(kbuf[kb & 1], s0, s1);
         if (k0 == 2) mask_tile(s0, j0);
         if (k1 == 2) mask_tile(s1, j0 + 32);
-        if (k0) pv_tile(s0, vbuf[kb & 1], 0);
-        if (k1) pv_tile(s1, vbuf[kb & 1], 1);
+        if (k0) pv_tile(s0, vbuf[kb & 1], 0, j0);
+        if (k1) pv_tile(s1, vbuf[kb & 1], 1, j0);
       }
+      if constexpr (PRECISE && TRAIN) usum = usum_pv + __shfl_xor(usum_pv, 32);
       if (!wave_ok) return;
       // accumulator value r of lane l: query q0 + crow(r), column 32 nt + l % 32
       E* O = static_cast<E*>(a.o) + (size_t)bh * n * D;

@@ -177,20 +177,27 @@ def test_dense_mode_validation():
     s, p = shape(), ea.default_params()
     f = ea._lib.entmax_attn_fwd_dense
     # null tau
-    assert f(s, p, _fake(), _fake(), _fake(), _fake(), None, _fake(), None, 0, None) == \
+    assert f(s, p, _fake(), _fake(), _fake(), _fake(), None, None, _fake(), None, 0, None) == \
         ea.EA_ERR_INVALID_ARG
     # o2 required while need_bwd
-    assert f(s, p, _fake(), _fake(), _fake(), _fake(), _fake(), None, None, 0, None) == \
+    assert f(s, p, _fake(), _fake(), _fake(), _fake(), _fake(), None, None, None, 0, None) == \
         ea.EA_ERR_INVALID_ARG
     # misaligned workspace
-    assert f(s, p, _fake(), _fake(), _fake(), _fake(), _fake(), _fake(), _fake() + 8, 64, None) == \
+    assert f(s, p, _fake(), _fake(), _fake(), _fake(), _fake(), None, _fake(), _fake() + 8, 64,
+             None) == ea.EA_ERR_INVALID_ARG
+    # fp32 inputs need tau_lo, forward and backward
+    s32 = shape(dt=ea.EA_F32)
+    assert f(s32, p, _fake(), _fake(), _fake(), _fake(), _fake(), None, _fake(), None, 0, None) == \
         ea.EA_ERR_INVALID_ARG
     b = ea._lib.entmax_attn_bwd_dense
     z = ea.entmax_attn_sizes(s, p)
     args = [_fake()] * 4
-    assert b(s, p, *args, _fake(), _fake(), _fake(), _fake(), _fake(), _fake(), z.ws_bwd - 4,
+    assert b(s, p, *args, _fake(), None, _fake(), _fake(), _fake(), _fake(), _fake(), z.ws_bwd - 4,
              None) == ea.EA_ERR_WORKSPACE
-    assert b(s, p, *args, None, _fake(), _fake(), _fake(), _fake(), _fake(), z.ws_bwd,
+    assert b(s, p, *args, None, None, _fake(), _fake(), _fake(), _fake(), _fake(), z.ws_bwd,
+             None) == ea.EA_ERR_INVALID_ARG
+    z32 = ea.entmax_attn_sizes(s32, p)
+    assert b(s32, p, *args, _fake(), None, _fake(), _fake(), _fake(), _fake(), _fake(), z32.ws_bwd,
              None) == ea.EA_ERR_INVALID_ARG
 
 
@@ -257,6 +264,11 @@ def test_binding_refuses_mismatched_dense_and_rows():
         ea.backward_dense(q, q, q, q, torch.zeros(2, 65), torch.zeros(1, 2, 64, 64))
     with pytest.raises(ValueError, match="o2 has dtype"):
         ea.backward_dense(q, q, q, q, torch.zeros(2, 64), q)
+    q32 = torch.zeros(1, 2, 64, 64)
+    with pytest.raises(ValueError, match="tau_lo"):
+        ea.backward_dense(q32, q32, q32, q32, torch.zeros(2, 64), q32)
+    with pytest.raises(ValueError, match="tau_lo has shape"):
+        ea.backward_dense(q32, q32, q32, q32, torch.zeros(2, 64), q32, tau_lo=torch.zeros(2, 63))
     s = torch.zeros(4, 100)
     with pytest.raises(ValueError, match="tau has shape"):
         ea.rows_backward(s, torch.zeros(5), torch.zeros(4, 100))
