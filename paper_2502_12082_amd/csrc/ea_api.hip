@@ -35,7 +35,11 @@ constexpr int MAX_ITER_CAP = 64;
 // two lists per row of a workgroup.
 constexpr int TAU_CACHE_CAP = 192;
 static_assert(TAU_CACHE_CAP % 16 == 0, "the solver reads lists in batches of 16 entries");
-constexpr size_t SOLVE_SLOT_BYTES = (size_t)TAU_CACHE_CAP * 2 * SOLVE_ROWS * sizeof(CandEntry);
+constexpr int SOLVE_QUAD_CAP = 96;
+static_assert(SOLVE_QUAD_CAP % 8 == 0, "the solver reads lists in batches of 8 quads");
+constexpr size_t SOLVE_SLOT_BYTES = solve_slot_bytes(SOLVE_QUAD_CAP);
+static_assert(SOLVE_SLOT_BYTES % (2 * SOLVE_THREADS * sizeof(CandEntry) * 8) == 0,
+              "a refilled slot holds a multiple of 8 single entries per list");
 constexpr size_t TAU_SLOT_BYTES = (size_t)TAU_CACHE_CAP * 2 * TAU_ROWS * sizeof(CandEntry);
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -94,7 +98,8 @@ int64_t cache_tiles(const Dims& d) { return d.BH * ((d.n + TAU_ROWS - 1) / TAU_R
 int64_t solve_slots(const Dims& d) {
   return solve_tiles(d) < MAX_SOLVE_SLOTS ? solve_tiles(d) : MAX_SOLVE_SLOTS;
 }
-static_assert(SOLVE_ROWS == 2 * TAU_ROWS, "a masked-path slot covers two fused-forward slots");
+static_assert(SOLVE_ROWS == 2 * TAU_ROWS && SOLVE_SLOT_BYTES >= 2 * TAU_SLOT_BYTES,
+              "a masked-path slot covers two fused-forward slots");
 
 void fill_sizes(const Dims& d, ea_sizes* z) {
   z->tau = (size_t)(d.BH * d.n) * 4;
@@ -246,9 +251,9 @@ ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const
     int64_t slots = workspace ? (int64_t)(ws_bytes / SOLVE_SLOT_BYTES) : 0;
     const int64_t most = solve_tiles(d);
     if (slots > most) slots = most;
-    CandEntry* cand = slots > 0 ? static_cast<CandEntry*>(workspace) : nullptr;
+    void* cand = slots > 0 ? workspace : nullptr;
     TauArgs ta{q, k, res->tau, res->block_mask, res->stats, nullptr, nullptr, nullptr, cand,
-               TAU_CACHE_CAP, (int)slots, /*tile0=*/0,
+               SOLVE_QUAD_CAP, (int)slots, /*tile0=*/0,
                (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma, params->causal,
                params->max_iter, params->tol, gk,
                const_cast<float*>(tau_lo_of(res, d)), c64_of(params), g64_of(params)};
@@ -416,7 +421,7 @@ ea_status entmax_attn_fwd_dense(const ea_shape* shape, const ea_params* params, 
   if (workspace && !aligned(workspace, 16)) return EA_ERR_INVALID_ARG;
   int64_t slots = workspace ? (int64_t)(ws_bytes / TAU_SLOT_BYTES) : 0;
   if (slots > cache_tiles(d)) slots = cache_tiles(d);
-  CandEntry* cand = slots > 0 ? static_cast<CandEntry*>(workspace) : nullptr;
+  void* cand = slots > 0 ? workspace : nullptr;
   const float c = (params->alpha - 1.0f) * params->scale;
   const float gamma = 1.0f / (params->alpha - 1.0f);
   TauArgs ta{q, k, tau, nullptr, nullptr, v, o, params->need_bwd ? o2 : nullptr, cand,

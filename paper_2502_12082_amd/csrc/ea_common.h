@@ -63,6 +63,15 @@ __device__ __forceinline__ float sum_halves(float v) {
   return lo + hi;
 }
 
+// max(a, b, c) in one v_max3_f32.  fmaxf chains on MFMA results also
+// canonicalise each operand (one more instruction per operand); scores are
+// finite or -inf, where the two agree.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 __device__ __forceinline__ f32x16 zero16() {
   f32x16 z;
 #pragma unroll

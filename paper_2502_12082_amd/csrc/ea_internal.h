@@ -16,8 +16,9 @@ constexpr int MAX_KEY_BLOCKS = MAX_SEQLEN / 64;
 // {1, 2, 4} run without transcendentals; 0 means general alpha.
 int gamma_kind(float alpha);
 
-// One cached score of the solver: the raw score s = <q_i, k_j> (the solver
-// forms x - tau from it exactly as in a streamed evaluation) and the key j.
+// One cached score of the no-mask forward's solver: the raw score
+// s = <q_i, k_j> (the solver forms x - tau from it exactly as in a streamed
+// evaluation) and the key j.
 struct alignas(8) CandEntry {
   float s;
   int32_t j;  // key index; its key block is j / 64
@@ -31,6 +32,20 @@ constexpr int SOLVE_THREADS = 256;
 constexpr int TAU_ROWS = 128;
 constexpr int TAU_THREADS = 256;
 
+// The masked path's solver caches quads: the four raw scores of four
+// consecutive keys 4 m .. 4 m + 3 that one lane holds for one row (16 bytes),
+// with m as a 16-bit key (2 bytes, in an array of their own).  Its first
+// evaluation copies the scores above the bracket's lower end into lists of
+// single scores (4 bytes, and their key blocks, 2 bytes).  A slot holds
+// `cap` quads and `cap` singles in each of the 2 * SOLVE_THREADS lists of a
+// workgroup.
+constexpr size_t SOLVE_QUAD_BYTES = 16 + 2;
+constexpr size_t SOLVE_SINGLE_BYTES = 4 + 2;
+constexpr size_t solve_slot_bytes(int cap) {
+  return (size_t)cap * 2 * SOLVE_THREADS * (SOLVE_QUAD_BYTES + SOLVE_SINGLE_BYTES);
+}
+static_assert(MAX_SEQLEN / 4 <= 65536, "a quad's key fits 16 bits");
+
 struct TauArgs {
   const void* q;
   const void* k;
@@ -42,8 +57,8 @@ struct TauArgs {
   const void* v;
   void* o;            // [BH, n, D] input dtype
   float* o2;          // [BH, n, D] fp32, or null (inference)
-  CandEntry* cand;    // candidate cache: one slot of 2 * rows * cap entries per workgroup, or null
-  int cap;            // entries per list
+  void* cand;         // candidate cache: one slot per workgroup (quads or CandEntry lists), or null
+  int cap;            // entries (quads for the masked path) per list
   int slots;          // cache slots (workgroup b of a launch uses slot b)
   int tile0;          // first tile of this launch (workgroup b solves tile tile0 + b)
   int BH, n, T;

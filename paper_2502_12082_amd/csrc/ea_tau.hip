@@ -69,8 +69,9 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
   // workspace has no slot for it.  A launch covers at most one tile per slot
   // (see launch_tiles).
   const int tile = a.tile0 + (int)blockIdx.x;
-  CandEntry* const cache =
-      a.cand && (int)blockIdx.x < a.slots ? a.cand + (size_t)blockIdx.x * a.cap * TAU_NT : nullptr;
+  CandEntry* const cache = a.cand && (int)blockIdx.x < a.slots
+                               ? static_cast<CandEntry*>(a.cand) + (size_t)blockIdx.x * a.cap * TAU_NT
+                               : nullptr;
 
   TileDma<TL, D, TAU_NT> dma;
   dma.init();
@@ -639,13 +640,27 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   const int TW = (T + 31) / 32;
   const float c = a.c, g = a.gamma;
   const bool newton_bound = g >= 1.f;  // f convex: Newton steps bound the root from below
-  // Tile a.tile0 + blockIdx.x, and this workgroup's cache slot: list (thread
-  // t, group gq) holds entry e at [(2 e + gq) * SV_NT + t]; null without a
-  // slot.  A launch covers at most one tile per slot (see launch_tiles).
+  // Tile a.tile0 + blockIdx.x, and this workgroup's cache slot, or none.  A
+  // launch covers at most one tile per slot (see launch_tiles).  List
+  // (thread t, group gq) holds entry e at index (2 e + gq) * SV_NT + t of
+  // each array of the slot.  The lists come in three forms:
+  //  - quads, as pass 0 collects them: a quad array (16 bytes per entry)
+  //    and its key array (2 bytes);
+  //  - compacted singles, written by the first cached evaluation from the
+  //    quads: a score array (4 bytes) and its key-block array (2 bytes)
+  //    after the quad arrays, so that the later evaluations read 4 bytes
+  //    per score and the quads stay intact;
+  //  - singles of a later fill (CandEntry, 8 bytes), up to `scap` per list
+  //    over the whole slot.
   const int tile = a.tile0 + (int)blockIdx.x;
-  CandEntry* const cache = a.cand && (int)blockIdx.x < a.slots
-                               ? a.cand + (size_t)blockIdx.x * a.cap * 2 * SV_NT
-                               : nullptr;
+  char* const slot = a.cand && (int)blockIdx.x < a.slots
+                         ? static_cast<char*>(a.cand) + (size_t)blockIdx.x * solve_slot_bytes(a.cap)
+                         : nullptr;
+  const bool cache = slot != nullptr;
+  char* const kslot = cache ? slot + (size_t)a.cap * 2 * SV_NT * 16 : nullptr;
+  char* const sslot = cache ? kslot + (size_t)a.cap * 2 * SV_NT * 2 : nullptr;
+  char* const bslot = cache ? sslot + (size_t)a.cap * 2 * SV_NT * 4 : nullptr;
+  const int scap = a.cap * (int)(SOLVE_QUAD_BYTES + SOLVE_SINGLE_BYTES) / (int)sizeof(CandEntry);
   const int bh = tile % a.BH;
   int qt = tile / a.BH;
   if (a.causal) qt = nqt - 1 - qt;  // longest rows first
@@ -771,19 +786,26 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   float kj[8];  // j^(-1/gamma)
 #pragma unroll
   for (int j = 0; j < 8; ++j) kj[j] = j == 0 ? 1.f : exp2f(-__log2f((float)(j + 1)) / g);
-  // Inserts the sub-tile's maximum into t4[gq] and returns it.
-  auto tile_max = [&](const f32x16& s, int gq) {
-    float v = fmaxf(s[0], s[1]);
+  // The maxima of the four quads of a sub-tile (scores r0 .. r0 + 3), and
+  // of the sub-tile from them.
+  auto quad_maxima = [&](const f32x16& s, float (&gm)[4]) {
 #pragma unroll
-    for (int r = 2; r < 16; r += 2) v = fmaxf(v, fmaxf(s[r], s[r + 1]));
-    const float top = v;
+    for (int r0 = 0; r0 < 16; r0 += 4)
+      gm[r0 / 4] = max3f(s[r0], s[r0 + 1], max3f(s[r0 + 2], s[r0 + 3], s[r0 + 3]));
+    return max3f(gm[0], gm[1], max3f(gm[2], gm[3], gm[3]));
+  };
+  // Inserts a sub-tile maximum into t4[gq].
+  auto insert_max = [&](float v, int gq) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float h = fmaxf(t4[gq][j], v);
       v = fminf(t4[gq][j], v);
       t4[gq][j] = h;
     }
-    return top;
+  };
+  auto tile_max = [&](const f32x16& s, int gq) {
+    float gm[4];
+    insert_max(quad_maxima(s, gm), gq);
   };
   // The row's eight largest sub-tile maxima, descending: the two lanes'
   // sorted lists merged by Batcher's odd-even network (the same result in
@@ -838,65 +860,164 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     return b - 1e-5f * fmaxf(fabsf(b), 1.f / c);
   };
 
-  int cc[2] = {0, 0};    // entries in this thread's two lists
+  int cc[2] = {0, 0};    // entries (quads, or singles of a later fill) in this thread's two lists
   int cmax[2] = {0, 0};  // wave maxima of cc once the cache is in use
-  // index of entry e of list gq of this thread (32-bit, from the
-  // workgroup-uniform slot base)
+  int ns[2] = {0, 0};    // compacted singles in this thread's two lists
+  int nsmax[2] = {0, 0}; // their wave maxima
+  // index of quad e of list gq of this thread
   constexpr uint32_t ENTRY_STEP = 2 * SV_NT;
   auto entry_idx = [&](int e, int gq) {
     return (uint32_t)e * ENTRY_STEP + (uint32_t)(gq * SV_NT + (int)threadIdx.x);
   };
-  auto put = [&](uint32_t idx, float sv, int jv) { cache[idx] = CandEntry{sv, jv}; };
-  // the same store at a 32-bit byte offset from the slot base (a wave-uniform
-  // base plus a per-lane offset needs no 64-bit address arithmetic)
-  auto put_at = [&](uint32_t byte_off, float sv, int jv) {
-    *reinterpret_cast<CandEntry*>(reinterpret_cast<char*>(cache) + byte_off) = CandEntry{sv, jv};
+  // Stores a quad and its key at index idx (32-bit byte offsets from the
+  // workgroup-uniform array bases need no 64-bit address arithmetic).
+  auto put = [&](uint32_t idx, const f32x4& v, int key4) {
+    *reinterpret_cast<f32x4*>(slot + idx * 16u) = v;
+    *reinterpret_cast<uint16_t*>(kslot + idx * 2u) = (uint16_t)key4;
   };
+  // the scores r0 .. r0 + 3 of a sub-tile (keys crow(r0) .. crow(r0) + 3)
+  auto quad_of = [](const f32x16& t, int r0) {
+    return f32x4{t[r0], t[r0 + 1], t[r0 + 2], t[r0 + 3]};
+  };
+  auto max4 = [](const f32x4& v) { return fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])); };
   auto wave_max = [&](int v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o));
     return v;
   };
-  // Reads list gq of this thread in batches of eight independent loads,
-  // up to the wave's longest list cmax rounded up to a multiple of 8.  That
-  // stays inside the slot (cmax <= cap, and cap is a multiple of 8); entries
-  // past this thread's own count are stale and never used.
-  // use(score, key) for each entry of list gq.
-  auto scan_entries = [&](int gq, auto&& use) {
+  // Reads list gq of this thread in batches of eight independent quad
+  // loads, up to the wave's longest list cmax rounded up to a multiple of 8.
+  // That stays inside the slot (cmax <= cap, and cap is a multiple of 8);
+  // quads past this thread's own count are stale and never used.
+  // use(quad, key) for each quad of list gq.
+  auto scan_quads = [&](int gq, auto&& use) {
+    for (int e0 = 0; e0 < cmax[gq]; e0 += 8) {
+      f32x4 qv[8];
+      int kv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t idx = entry_idx(e0 + u, gq);
+        qv[u] = *reinterpret_cast<const f32x4*>(slot + idx * 16u);
+        kv[u] = *reinterpret_cast<const uint16_t*>(kslot + idx * 2u);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (e0 + u < cc[gq]) use(qv[u], kv[u]);
+    }
+  };
+  // The scores of both lists for an evaluation: eight quads from each list
+  // per batch, up to the longer wave maximum rounded up to 8.  use(gq, score)
+  // in list order.
+  auto scan_scores = [&](auto&& use) {
+    const int m = max(cmax[0], cmax[1]);
+    for (int e0 = 0; e0 < m; e0 += 8) {
+      f32x4 v0[8], v1[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        v0[u] = *reinterpret_cast<const f32x4*>(slot + entry_idx(e0 + u, 0) * 16u);
+        v1[u] = *reinterpret_cast<const f32x4*>(slot + entry_idx(e0 + u, 1) * 16u);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (e0 + u < cc[0]) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) use(0, v0[u][i]);
+        }
+        if (e0 + u < cc[1]) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) use(1, v1[u][i]);
+        }
+      }
+    }
+  };
+  // The compacted singles of both lists for an evaluation (4-byte loads).
+  auto scan_scores_compact = [&](auto&& use) {
+    const int m = max(nsmax[0], nsmax[1]);
+    for (int e0 = 0; e0 < m; e0 += 8) {
+      float v0[8], v1[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        v0[u] = *reinterpret_cast<const float*>(sslot + entry_idx(e0 + u, 0) * 4u);
+        v1[u] = *reinterpret_cast<const float*>(sslot + entry_idx(e0 + u, 1) * 4u);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (e0 + u < ns[0]) use(0, v0[u]);
+        if (e0 + u < ns[1]) use(1, v1[u]);
+      }
+    }
+  };
+  // The compacted singles of list gq with their key blocks: use(score, kb).
+  auto scan_compact = [&](int gq, auto&& use) {
+    for (int e0 = 0; e0 < nsmax[gq]; e0 += 8) {
+      float v[8];
+      int kv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t idx = entry_idx(e0 + u, gq);
+        v[u] = *reinterpret_cast<const float*>(sslot + idx * 4u);
+        kv[u] = *reinterpret_cast<const uint16_t*>(bslot + idx * 2u);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (e0 + u < ns[gq]) use(v[u], kv[u]);
+    }
+  };
+  // The quads of both lists with their keys: use(gq, quad, key).
+  auto scan_quads_both = [&](auto&& use) {
+    const int m = max(cmax[0], cmax[1]);
+    for (int e0 = 0; e0 < m; e0 += 8) {
+      f32x4 v0[8], v1[8];
+      int k0[8], k1[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i0 = entry_idx(e0 + u, 0), i1 = entry_idx(e0 + u, 1);
+        v0[u] = *reinterpret_cast<const f32x4*>(slot + i0 * 16u);
+        v1[u] = *reinterpret_cast<const f32x4*>(slot + i1 * 16u);
+        k0[u] = *reinterpret_cast<const uint16_t*>(kslot + i0 * 2u);
+        k1[u] = *reinterpret_cast<const uint16_t*>(kslot + i1 * 2u);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (e0 + u < cc[0]) use(0, v0[u], k0[u]);
+        if (e0 + u < cc[1]) use(1, v1[u], k1[u]);
+      }
+    }
+  };
+  // Lists of singles of a later fill: use(score, key).
+  auto scan_singles = [&](int gq, auto&& use) {
     for (int e0 = 0; e0 < cmax[gq]; e0 += 8) {
       CandEntry ce[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) ce[u] = cache[entry_idx(e0 + u, gq)];
+      for (int u = 0; u < 8; ++u) ce[u] = *reinterpret_cast<const CandEntry*>(slot + entry_idx(e0 + u, gq) * 8u);
 #pragma unroll
       for (int u = 0; u < 8; ++u)
         if (e0 + u < cc[gq]) use(ce[u].s, ce[u].j);
     }
   };
-  // The scores of both lists for an evaluation: sixteen independent 4-byte
-  // loads from each list per batch, up to the longer wave maximum rounded up
-  // to 16 (inside the slot: cap is a multiple of 16).  use(gq, score).
-  auto scan_scores = [&](auto&& use) {
+  auto scan_scores_singles = [&](auto&& use) {
     const int m = max(cmax[0], cmax[1]);
-    for (int e0 = 0; e0 < m; e0 += 16) {
-      float v0[16], v1[16];
+    for (int e0 = 0; e0 < m; e0 += 8) {
+      float v0[8], v1[8];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        v0[u] = cache[entry_idx(e0 + u, 0)].s;
-        v1[u] = cache[entry_idx(e0 + u, 1)].s;
+      for (int u = 0; u < 8; ++u) {
+        v0[u] = reinterpret_cast<const CandEntry*>(slot + entry_idx(e0 + u, 0) * 8u)->s;
+        v1[u] = reinterpret_cast<const CandEntry*>(slot + entry_idx(e0 + u, 1) * 8u)->s;
       }
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
+      for (int u = 0; u < 8; ++u) {
         if (e0 + u < cc[0]) use(0, v0[u]);
         if (e0 + u < cc[1]) use(1, v1[u]);
       }
     }
   };
-  // Keeps the entries of list gq above `sb` (all lanes of the wave).
-  auto filter = [&](int gq, float sb) {
+  // Keeps the quads of list gq with a score above `sb` (all lanes of the
+  // wave).  In place: a quad moves only to a position already read.
+  auto filter = [&](int gq, float sbv) {
     cmax[gq] = wave_max(cc[gq]);
     int k = 0;
-    scan_entries(gq, [&](float sv, int kv) {
-      if (sv > sb) put(entry_idx(k++, gq), sv, kv);
+    scan_quads(gq, [&](const f32x4& v, int key4) {
+      if (max4(v) > sbv) put(entry_idx(k++, gq), v, key4);
     });
     cc[gq] = k;
   };
@@ -972,19 +1093,14 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     f32x16 s[2][2];
     int k[2][2];
     if (!block(kb, kt, s, k)) return;
-    float tm[2][2];
+    float tm[2][2], gm[2][2][4];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int gq = 0; gq < 2; ++gq) {
-        if (kb >= W) {
-          tm[h][gq] = k[h][gq] ? tile_max(s[h][gq], gq) : -INFINITY;
-        } else {
-          float v = s[h][gq][0];
-#pragma unroll
-          for (int r = 1; r < 16; ++r) v = fmaxf(v, s[h][gq][r]);
-          tm[h][gq] = k[h][gq] ? v : -INFINITY;
-        }
+        const float v = quad_maxima(s[h][gq], gm[h][gq]);
+        tm[h][gq] = k[h][gq] ? v : -INFINITY;
+        if (kb >= W && k[h][gq]) insert_max(v, gq);
       }
     if (!cache || fill_dead) return;
     // Every 4 blocks the running bound takes the one-term bound of the
@@ -999,45 +1115,34 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         if (row_ok[gq]) sb[gq] = fmaxf(sb[gq], score_bound(u, (kb & 31) == 0));
       }
     }
-    // a block adds at most 32 entries to each list
+    // a block adds at most 8 quads to each list
 #pragma unroll
     for (int gq = 0; gq < 2; ++gq) {
-      if (__ballot(cc[gq] > a.cap - 32) != 0ull) {
+      if (__ballot(cc[gq] > a.cap - 8) != 0ull) {
         filter(gq, sb[gq]);
-        if (__ballot(cc[gq] > a.cap - 32) != 0ull) {
+        if (__ballot(cc[gq] > a.cap - 8) != 0ull) {
           fill_dead = 1;
           return;
         }
       }
     }
-    // Only sub-tiles whose maximum passes in some lane are searched, and in
-    // them only the groups of four scores whose maximum passes in some lane
-    // (most searched sub-tiles hold one entry in one lane: the per-score
-    // tests of the other groups would cost the whole wave).  The entries keep
-    // the stream's order.  (Measured against one test per score: the solver
-    // takes 8-10% less at c = 16 and at n = 65536 causal, d = 64, and 3% more
-    // at c = 1, where most groups of a searched sub-tile pass.)
+    // Only sub-tiles whose maximum passes in some lane are searched; in them
+    // each lane appends the quads holding a score above the bound, with one
+    // 16-byte store per quad instead of one store per score.  The scores of
+    // a quad below the bound are 0 at every tau of the bracket, as in a
+    // streamed pass.  The quads keep the stream's order.
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int gq = 0; gq < 2; ++gq)
         if (__ballot(tm[h][gq] > sb[gq]) != 0ull) {
-          const f32x16& t = s[h][gq];
-          constexpr uint32_t STEP_BYTES = ENTRY_STEP * sizeof(CandEntry);
-          uint32_t off = entry_idx(cc[gq], gq) * (uint32_t)sizeof(CandEntry);
 #pragma unroll
           for (int r0 = 0; r0 < 16; r0 += 4) {
-            const float m4 = fmaxf(fmaxf(t[r0], t[r0 + 1]), fmaxf(t[r0 + 2], t[r0 + 3]));
-            if (__ballot(m4 > sb[gq]) == 0ull) continue;
-#pragma unroll
-            for (int r = r0; r < r0 + 4; ++r) {
-              if (t[r] > sb[gq]) {
-                put_at(off, t[r], kb * BLK + 32 * h + crow(r));
-                off += STEP_BYTES;
-              }
+            if (gm[h][gq][r0 / 4] > sb[gq]) {
+              put(entry_idx(cc[gq], gq), quad_of(s[h][gq], r0), (kb * BLK + 32 * h + crow(r0)) >> 2);
+              ++cc[gq];
             }
           }
-          cc[gq] = (int)((off / (uint32_t)sizeof(CandEntry) - entry_idx(0, gq)) / ENTRY_STEP);
         }
   });
 
@@ -1069,6 +1174,8 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     for (int gq = 0; gq < 2; ++gq) cmax[gq] = wave_max(cc[gq]);
   }
   int attempts = cache ? 1 : 0;  // cache fills tried (pass 0 is the first)
+  // form of the lists: 0 quads, 1 compacted singles, 2 singles of a later fill
+  int lists = 0;
   bool fits = false;             // a fill at the current lower end would fit
   float f_prev[2] = {INFINITY, INFINITY};
 
@@ -1142,18 +1249,22 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       const float t0 = lo[gq] / c;
       s_lo[gq] = row_ok[gq] ? t0 - 1e-6f * fmaxf(fabsf(t0), 1.f / c) : INFINITY;
     }
+    // (this fill stores single scores: after an evaluation the bracket is
+    // narrow and few scores of a quad are above its lower end)
     auto fill_tile = [&](const f32x16& s, int gq, int jb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         if (s[r] > s_lo[gq]) {
-          if (cc[gq] < a.cap) put(entry_idx(cc[gq], gq), s[r], jb + crow(r));
+          if (cc[gq] < scap)
+            *reinterpret_cast<CandEntry*>(slot + entry_idx(cc[gq], gq) * 8u) = CandEntry{s[r], jb + crow(r)};
           ++cc[gq];
         }
       }
     };
     auto fill_done = [&]() {
-      if (!__syncthreads_or(cc[0] > a.cap || cc[1] > a.cap)) {
+      if (!__syncthreads_or(cc[0] > scap || cc[1] > scap)) {
         cached = true;
+        lists = 2;
         cmax[0] = wave_max(cc[0]);
         cmax[1] = wave_max(cc[1]);
       }
@@ -1211,8 +1322,38 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       });
       ++passes;
       if (count) {
-        fits = !__syncthreads_or(over[0] > a.cap || over[1] > a.cap);
+        fits = !__syncthreads_or(over[0] > scap || over[1] > scap);
         if (!fits) attempts = 2;  // no retry, and no more counting
+      }
+    } else if (lists == 2) {
+      scan_scores_singles([&](int gq, float sv) { add_z(relu_z(c, sv, tau[gq]), gq); });
+    } else if (lists == 1) {
+      scan_scores_compact([&](int gq, float sv) { add_z(relu_z(c, sv, tau[gq]), gq); });
+    } else if (it == 0) {
+      // first evaluation on the quads: also copies the scores above the
+      // lower end (every later tau stays >= lo, so the others are 0 there)
+      // into the compacted lists, in the same order
+      int cs[2] = {0, 0};
+      scan_quads_both([&](int gq, const f32x4& v, int key4) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          add_z(relu_z(c, v[i], tau[gq]), gq);
+          if (v[i] > s_lo[gq]) {
+            if (cs[gq] < a.cap) {
+              const uint32_t idx = entry_idx(cs[gq], gq);
+              *reinterpret_cast<float*>(sslot + idx * 4u) = v[i];
+              *reinterpret_cast<uint16_t*>(bslot + idx * 2u) = (uint16_t)(key4 >> 4);
+            }
+            ++cs[gq];
+          }
+        }
+      });
+      if (!__syncthreads_or(cs[0] > a.cap || cs[1] > a.cap)) {
+        lists = 1;
+        ns[0] = cs[0];
+        ns[1] = cs[1];
+        nsmax[0] = wave_max(ns[0]);
+        nsmax[1] = wave_max(ns[1]);
       }
     } else {
       scan_scores([&](int gq, float sv) { add_z(relu_z(c, sv, tau[gq]), gq); });
@@ -1293,9 +1434,16 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     // use(group, fp32 score, key) for every valid entry of this lane's rows:
     // from the lists when they hold every candidate, else from a K pass
     auto visit = [&](auto&& use) {
-      if (cached) {
+      if (cached && lists == 2) {
 #pragma unroll
-        for (int gq = 0; gq < 2; ++gq) scan_entries(gq, [&](float sv, int jv) { use(gq, sv, jv); });
+        for (int gq = 0; gq < 2; ++gq) scan_singles(gq, [&](float sv, int jv) { use(gq, sv, jv); });
+      } else if (cached) {
+#pragma unroll
+        for (int gq = 0; gq < 2; ++gq)
+          scan_quads(gq, [&](const f32x4& v, int key4) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) use(gq, v[i], 4 * key4 + i);
+          });
       } else {
         stream([&](int kb, const E* kt) {
           f32x16 s[2][2];
@@ -1373,11 +1521,30 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
       __syncthreads();
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq)
-        scan_entries(gq, [&](float sv, int jv) {
-          const int kv = jv >> 6;
-          if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+      for (int gq = 0; gq < 2; ++gq) {
+        if (lists == 2) {
+          scan_singles(gq, [&](float sv, int jv) {
+            const int kv = jv >> 6;
+            if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+          });
+          continue;
+        }
+        if (lists == 1) {
+          scan_compact(gq, [&](float sv, int kv) {
+            if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+          });
+          continue;
+        }
+        scan_quads(gq, [&](const f32x4& v, int key4) {
+          bool any = false;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) any |= in_support(relu_z(c, v[i], tau[gq])) != 0;
+          if (any) {
+            const int kv = key4 >> 4;  // key block of the quad
+            atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+          }
         });
+      }
     }
   }
   __syncthreads();

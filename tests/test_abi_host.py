@@ -54,9 +54,10 @@ def test_sizes():
     assert z.q_count == z.k_count == BH * T * 4
     assert z.q_index == z.k_index == BH * T * T * 4
     assert z.stats == 2 * BH * T * 4
-    # solver cache: one slot per 256-row tile, each 2 lists x 192 entries x
-    # 256 threads x 8 bytes, at most 512 slots
-    slot = 2 * 192 * 256 * 8
+    # solver cache: one slot per 256-row tile, each 2 lists x 256 threads x
+    # 96 quads (16 bytes of scores + 2 bytes of key) and 96 singles (4 bytes
+    # of score + 2 bytes of key block), at most 512 slots
+    slot = 2 * 256 * 96 * (18 + 6)
     assert z.ws_fwd == BH * ((n + 255) // 256) * slot and z.ws_bwd == BH * n * 4
     big = ea.entmax_attn_sizes(ea.Shape(1, 8, 65536, 64, 0), p)
     assert big.ws_fwd == 512 * slot  # 2048 tiles share 512 slots

@@ -102,7 +102,7 @@ def test_partial_workspace():
     (down to a single workgroup for all 12 tiles); a workspace too small for
     one slot streams K.  Results equal streaming either way."""
     inp = synth.attention_inputs(2, 2, 1500, 128, c=1.0, dtype="bf16", seed=8)
-    slot = 2 * 192 * 256 * 8  # bytes of one slot
+    slot = 2 * 96 * 256 * (18 + 6)  # bytes of one slot
     for slots in (4, 1, 0):
         (o0, r0), (o1, r1) = _both(inp, 1.5, True, ws_bytes=max(16, slots * slot))
         dt = ((r1.tau.double() - r0.tau.double()).abs() / r0.tau.double().abs().clamp(min=1.0))
