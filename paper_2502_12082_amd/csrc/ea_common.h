@@ -72,6 +72,14 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
   return r;
 }
 
+// Buffer resource over `bytes` bytes at p (gfx9 layout: raw byte
+// addressing).  A buffer access at a byte offset >= `bytes` is dropped by the
+// hardware, which turns predicated stores into unconditional ones.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)bytes, 0x00020000);
+}
+constexpr uint32_t BUFFER_OOB = 0x80000000u;  // an offset past every buffer here
+
 __device__ __forceinline__ f32x16 zero16() {
   f32x16 z;
 #pragma unroll

@@ -1333,19 +1333,25 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       // first evaluation on the quads: also copies the scores above the
       // lower end (every later tau stays >= lo, so the others are 0 there)
       // into the compacted lists, in the same order
+      // Each score is stored unconditionally through buffer resources that
+      // end with the compacted arrays: a score that stays out, or one past
+      // the capacity, gets an offset past the end and its stores are
+      // dropped (no branches, one increment of the count).
       int cs[2] = {0, 0};
+      const uint32_t sbytes = (uint32_t)a.cap * 2 * SV_NT * 4;
+      const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(sslot, sbytes), rk = buffer_rsrc(bslot, sbytes / 2);
       scan_quads_both([&](int gq, const f32x4& v, int key4) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          add_z(relu_z(c, v[i], tau[gq]), gq);
-          if (v[i] > s_lo[gq]) {
-            if (cs[gq] < a.cap) {
-              const uint32_t idx = entry_idx(cs[gq], gq);
-              *reinterpret_cast<float*>(sslot + idx * 4u) = v[i];
-              *reinterpret_cast<uint16_t*>(bslot + idx * 2u) = (uint16_t)(key4 >> 4);
-            }
-            ++cs[gq];
-          }
+          const float x = v[i];
+          add_z(relu_z(c, x, tau[gq]), gq);
+          const bool keep = x > s_lo[gq];
+          const uint32_t off = keep ? entry_idx(cs[gq], gq) * 4u : BUFFER_OOB;
+          // (__float_as_uint of a named float: a bit cast of the vector
+          // element itself stored element 0 for every i)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), rs, off, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(key4 >> 4), rk, off >> 1, 0, 0);
+          cs[gq] += keep ? 1 : 0;
         }
       });
       if (!__syncthreads_or(cs[0] > a.cap || cs[1] > a.cap)) {
