@@ -135,3 +135,29 @@ def test_cache_retry_after_overflow():
     assert do <= BF16_TOL
     assert retried > 0
     assert (s1 <= s0 + 2).all()
+
+
+def test_cache_uncompacted_quads():
+    """Keys repeated in groups of four, aligned with the quads of the lists,
+    so every cached quad holds four equal scores.  At c = 0.8 the quads of
+    every list fit (the max pass does not overflow), while the scores above
+    the lower end of the bracket outnumber the 96 singles of a list: the
+    first cached evaluation cannot compact them, and the evaluations and the
+    mask rebuild of every tile run on the quads themselves (checked once with
+    an instrumented build).  tau, O and the mask match streaming (every tile
+    on its cache, one K pass) and the oracle."""
+    inp = synth.attention_inputs(1, 2, 2048, 64, c=0.8, dtype="bf16", with_dout=True, seed=77)
+    inp["k"] = synth.Tensor(np.repeat(inp["k"].raw[:, :, ::4, :], 4, axis=2), "bf16")
+    (o0, r0), (o1, r1) = _both(inp, 1.5, False)
+    dt = ((r1.tau.double() - r0.tau.double()).abs() / r0.tau.double().abs().clamp(min=1.0)).max().item()
+    passes = r1.stats[0].cpu().numpy()
+    log("quads: dtau %.2e, K passes (cached) %.2f" % (dt, passes.mean()))
+    assert dt <= 1e-4
+    assert (o1.float() - o0.float()).abs().max().item() <= BF16_TOL
+    assert torch.equal(r0.block_mask, r1.block_mask)
+    assert (passes == 1).all()
+    gpu = run_gpu(inp, 1.5, 64 ** -0.5, False, True)
+    check_tables(gpu, False)
+    for bh in range(2):
+        ref = oracle_head(inp, bh, 1.5, 64 ** -0.5, False, True)
+        log("  errors %s" % check_head(gpu, ref, bh, "bf16", "quads bh=%d" % bh))
