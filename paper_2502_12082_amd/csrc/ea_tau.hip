@@ -706,6 +706,20 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     __syncthreads();  // the next pass refills buffer 0
   };
   auto stream = [&](auto&& body) { stream_n(nkb, body); };
+  // Streams every key block once, starting at block `first` and wrapping
+  // around.
+  auto stream_from = [&](int first, auto&& body) {
+    dma.issue(kbuf[0], K, first * BLK, n);
+    for (int i = 0; i < nkb; ++i) {
+      const int kb = first + i < nkb ? first + i : first + i - nkb;
+      const int nx = kb + 1 < nkb ? kb + 1 : 0;
+      dma_wait();
+      __syncthreads();
+      if (i + 1 < nkb) dma.issue(kbuf[(i + 1) & 1], K, nx * BLK, n);
+      body(kb, kbuf[i & 1]);
+    }
+    __syncthreads();  // the next pass refills buffer 0
+  };
 
   // S^T sub-tiles of the staged block: s[h][gq] = keys [32 h, 32 h + 32) x
   // query group gq; value r of lane l is key 32 h + crow(r), query l % 32 of
@@ -1028,8 +1042,11 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // their sub-tile maxima, so that the collection below starts from a bound
   // close to its final value instead of collecting (and later dropping) most
   // scores of its first blocks.  Those blocks' maxima are then not inserted
-  // again (the bound needs distinct keys).  The stream covers an eighth or
-  // half of the key blocks.  After the eighth it counts the threads holding
+  // again (the bound needs distinct keys).  The stream covers an eighth of
+  // the key blocks, or else half of them (all of them at d = 64, where a
+  // block's products cost half as much against the collection work they
+  // save: the encoder shape, n = 1024, took 0.147 against 0.183 ms).  After
+  // the eighth it counts the threads holding
   // a score of the last block above the bound of the maxima so far, and
   // stops there if at most WARM_STOP of them do: for rows with few large
   // scores the collection is cheap and a longer stream only adds MFMA work,
@@ -1040,7 +1057,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // threads at c = 1, 95 at c = 2, 49 at c = 4 and 23 at c = 16.)
   int W = 0;
   if (cache) {
-    const int w_lo = max(1, nkb / 8), w_hi = max(1, nkb / 2);
+    const int w_lo = max(1, nkb / 8), w_hi = D <= 64 ? nkb : max(1, nkb / 2);
     dma.issue(kbuf[0], K, 0, n);
     for (int kb = 0;; ++kb) {
       dma_wait();
@@ -1086,7 +1103,10 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       sb[gq] = row_ok[gq] ? score_bound(u, true) : INFINITY;
     }
   }
-  stream([&](int kb, const E* kt) {
+  // The collection starts after the first stream's blocks, whose maxima are
+  // in, and takes them last, at the bound of all the others: fewer of their
+  // scores pass than at the bound of the first stream alone.
+  stream_from(W < nkb ? W : 0, [&](int kb, const E* kt) {
     // once the lists have overflowed, the first stream's blocks need nothing
     // more (their maxima are in)
     if (kb < W && fill_dead) return;
