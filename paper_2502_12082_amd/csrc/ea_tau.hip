@@ -616,33 +616,43 @@ __global__ __launch_bounds__(TAU_NT, 2) void tau_solve_kernel(TauArgs a) {
 constexpr int SV_WAVES = SOLVE_THREADS / 64;
 constexpr int SV_NT = SOLVE_THREADS;
 constexpr int SV_ROWS = SOLVE_ROWS;
+// waves per SIMD for the one-group form (G = 1) of solve_kernel, and the
+// grids that use it: fewer 256-row tiles than two per compute unit
+constexpr int SV_OCC1 = 3;
+constexpr int SV_G1_BELOW = 512;
 // threads (of SV_NT) with a score above the running bound in one key block
 // at or below which the solver's first stream ends early
 constexpr int WARM_STOP = SV_NT / 2;
-static_assert(SV_ROWS == 64 * SV_WAVES, "one 64-row query block per wave");
+static_assert(SV_ROWS == 64 * SV_WAVES, "one 64-row query block per wave (G = 2)");
 
+// G = 2: each wave owns one 64-row query block as two groups of 32 rows.
+// G = 1 (small grids): each wave owns 32 rows, two waves share a query
+// block, and the workgroup covers 128 rows: twice the waves for the same
+// work, with half the state each, so that more of them share each SIMD.
 // fp32 operands at d = 128 (128 registers of query fragments) run one wave
-// per SIMD; every other variant fits two.
-template <typename E, int D, int GK>
-__global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void solve_kernel(TauArgs a) {
+// per SIMD with G = 2.
+template <typename E, int D, int GK, int G>
+__global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 128 ? 1 : 2)) void solve_kernel(TauArgs a) {
   using TL = PadTile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
-  constexpr int BW = MAX_KEY_BLOCKS / 32;  // mask words per wave
+  constexpr int BW = MAX_KEY_BLOCKS / 32;  // mask words per query block
+  constexpr int ROWS = SV_WAVES * 32 * G;  // rows per workgroup
   __shared__ __attribute__((aligned(16))) E kbuf[2][TL::ELEMS];
   // bit kb of word kb / 32: key block kb holds a positive probability for a
-  // row of the wave's query block
+  // row of the query block (one per wave with G = 2, per pair of waves with
+  // G = 1)
   __shared__ uint32_t bits[SV_WAVES * BW];
 
   const int lane = lane_id(), w = wave_id();
   const int n = a.n, T = a.T;
-  const int nqt = (n + SV_ROWS - 1) / SV_ROWS;
+  const int nqt = (n + ROWS - 1) / ROWS;
   const int TW = (T + 31) / 32;
   const float c = a.c, g = a.gamma;
   const bool newton_bound = g >= 1.f;  // f convex: Newton steps bound the root from below
   // Tile a.tile0 + blockIdx.x, and this workgroup's cache slot, or none.  A
   // launch covers at most one tile per slot (see launch_tiles).  List
-  // (thread t, group gq) holds entry e at index (2 e + gq) * SV_NT + t of
+  // (thread t, group gq) holds entry e at index (G e + gq) * SV_NT + t of
   // each array of the slot.  The lists come in three forms:
   //  - quads, as pass 0 collects them: a quad array (16 bytes per entry)
   //    and its key array (2 bytes);
@@ -654,42 +664,44 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   //    over the whole slot.
   const int tile = a.tile0 + (int)blockIdx.x;
   char* const slot = a.cand && (int)blockIdx.x < a.slots
-                         ? static_cast<char*>(a.cand) + (size_t)blockIdx.x * solve_slot_bytes(a.cap)
+                         ? static_cast<char*>(a.cand) + (size_t)blockIdx.x * (solve_slot_bytes(a.cap) / 2 * G)
                          : nullptr;
   const bool cache = slot != nullptr;
-  char* const kslot = cache ? slot + (size_t)a.cap * 2 * SV_NT * 16 : nullptr;
-  char* const sslot = cache ? kslot + (size_t)a.cap * 2 * SV_NT * 2 : nullptr;
-  char* const bslot = cache ? sslot + (size_t)a.cap * 2 * SV_NT * 4 : nullptr;
+  char* const kslot = cache ? slot + (size_t)a.cap * G * SV_NT * 16 : nullptr;
+  char* const sslot = cache ? kslot + (size_t)a.cap * G * SV_NT * 2 : nullptr;
+  char* const bslot = cache ? sslot + (size_t)a.cap * G * SV_NT * 4 : nullptr;
   const int scap = a.cap * (int)(SOLVE_QUAD_BYTES + SOLVE_SINGLE_BYTES) / (int)sizeof(CandEntry);
   const int bh = tile % a.BH;
   int qt = tile / a.BH;
   if (a.causal) qt = nqt - 1 - qt;  // longest rows first
-  const int qb = qt * SV_WAVES + w;
-  const int q0 = qb * BLK;
+  const int q0 = qt * ROWS + 32 * G * w;  // first row of this wave
+  const int qb = q0 / BLK;                 // its query block
+  const int qbl = G == 2 ? w : w >> 1;     // that block's mask words in `bits`
+  const bool writer = G == 2 || (w & 1) == 0;  // writes the block's mask and stats
   const bool wave_ok = q0 < n;
-  int qi[2], ni[2];
-  bool row_ok[2];
+  int qi[G], ni[G];
+  bool row_ok[G];
 #pragma unroll
-  for (int gq = 0; gq < 2; ++gq) {
+  for (int gq = 0; gq < G; ++gq) {
     qi[gq] = q0 + 32 * gq + (lane & 31);
     row_ok[gq] = qi[gq] < n;
     ni[gq] = a.causal ? qi[gq] + 1 : n;
   }
   const E* Q = static_cast<const E*>(a.q) + (size_t)bh * n * D;
   const E* K = static_cast<const E*>(a.k) + (size_t)bh * n * D;
-  const int wg_last = min(n, (qt + 1) * SV_ROWS) - 1;
+  const int wg_last = min(n, (qt + 1) * ROWS) - 1;
   const int nkb = a.causal ? wg_last / BLK + 1 : T;
 
   TileDma<TL, D, SV_NT> dma;
   dma.init();
 
-  typename M::frag qf[2][KS];
+  typename M::frag qf[G][KS];
 #pragma unroll
-  for (int gq = 0; gq < 2; ++gq)
+  for (int gq = 0; gq < G; ++gq)
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) qf[gq][kk] = load_row_frag_global<E, D>(Q, qi[gq], n, kk);
 
-  for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
+  for (int x = lane; x < TW; x += 64) bits[qbl * BW + x] = 0;
 
   // Streams every key block in order, double-buffered: block kb + 1 is
   // copied into LDS while body(kb, tile) works on block kb.  The candidate
@@ -724,20 +736,20 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // S^T sub-tiles of the staged block: s[h][gq] = keys [32 h, 32 h + 32) x
   // query group gq; value r of lane l is key 32 h + crow(r), query l % 32 of
   // the group.  Four independent accumulation chains.
-  auto scores = [&](const E* kt, f32x16 (&s)[2][2]) {
+  auto scores = [&](const E* kt, f32x16 (&s)[2][G]) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      s[h][0] = zero16();
-      s[h][1] = zero16();
-    }
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int gq = 0; gq < G; ++gq) s[h][gq] = zero16();
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       const typename M::frag a0 = lds_row_frag_pad<E, D>(kt, (lane & 31), kk);
       const typename M::frag a1 = lds_row_frag_pad<E, D>(kt, 32 + (lane & 31), kk);
-      s[0][0] = M::mma(a0, qf[0][kk], s[0][0]);
-      s[0][1] = M::mma(a0, qf[1][kk], s[0][1]);
-      s[1][0] = M::mma(a1, qf[0][kk], s[1][0]);
-      s[1][1] = M::mma(a1, qf[1][kk], s[1][1]);
+#pragma unroll
+      for (int gq = 0; gq < G; ++gq) {
+        s[0][gq] = M::mma(a0, qf[gq][kk], s[0][gq]);
+        s[1][gq] = M::mma(a1, qf[gq][kk], s[1][gq]);
+      }
     }
   };
   // Sub-tile state: 0 = nothing valid, 1 = all valid, 2 = per-element masking.
@@ -758,13 +770,13 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   };
   // The block's sub-tiles, scored and masked; returns the kinds (k[h][gq]),
   // or false when the wave has nothing valid in the block.
-  auto block = [&](int kb, const E* kt, f32x16 (&s)[2][2], int (&k)[2][2]) {
+  auto block = [&](int kb, const E* kt, f32x16 (&s)[2][G], int (&k)[2][G]) {
     const int j0 = kb * BLK;
     bool anyv = false, all1 = true;
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq) {
+      for (int gq = 0; gq < G; ++gq) {
         k[h][gq] = sub_kind(j0 + 32 * h, gq);
         anyv |= k[h][gq] != 0;
         all1 &= k[h][gq] == 1;
@@ -775,7 +787,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int gq = 0; gq < 2; ++gq)
+        for (int gq = 0; gq < G; ++gq)
           if (k[h][gq] == 2) mask_tile(s[h][gq], j0 + 32 * h, gq);
     }
     return true;
@@ -792,9 +804,9 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // below.  A wave whose lists come near their capacity filters them by the
   // current bound; if that frees too little, the workgroup stops collecting
   // and its evaluations stream K.
-  float t4[2][4];
+  float t4[G][4];
 #pragma unroll
-  for (int gq = 0; gq < 2; ++gq)
+  for (int gq = 0; gq < G; ++gq)
 #pragma unroll
     for (int j = 0; j < 4; ++j) t4[gq][j] = -INFINITY;
   float kj[8];  // j^(-1/gamma)
@@ -874,12 +886,12 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     return b - 1e-5f * fmaxf(fabsf(b), 1.f / c);
   };
 
-  int cc[2] = {0, 0};    // entries (quads, or singles of a later fill) in this thread's two lists
-  int cmax[2] = {0, 0};  // wave maxima of cc once the cache is in use
-  int ns[2] = {0, 0};    // compacted singles in this thread's two lists
-  int nsmax[2] = {0, 0}; // their wave maxima
+  int cc[G] = {};    // entries (quads, or singles of a later fill) in this thread's two lists
+  int cmax[G] = {};  // wave maxima of cc once the cache is in use
+  int ns[G] = {};    // compacted singles in this thread's two lists
+  int nsmax[G] = {}; // their wave maxima
   // index of quad e of list gq of this thread
-  constexpr uint32_t ENTRY_STEP = 2 * SV_NT;
+  constexpr uint32_t ENTRY_STEP = G * SV_NT;
   auto entry_idx = [&](int e, int gq) {
     return (uint32_t)e * ENTRY_STEP + (uint32_t)(gq * SV_NT + (int)threadIdx.x);
   };
@@ -898,6 +910,19 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o));
     return v;
+  };
+  auto max_over = [](const int (&v)[G]) {
+    int m = v[0];
+#pragma unroll
+    for (int gq = 1; gq < G; ++gq) m = max(m, v[gq]);
+    return m;
+  };
+  // whether v[gq] > limit for some group
+  auto any_over = [](const int (&v)[G], int limit) {
+    bool r = false;
+#pragma unroll
+    for (int gq = 0; gq < G; ++gq) r |= v[gq] > limit;
+    return r;
   };
   // Reads list gq of this thread in batches of eight independent quad
   // loads, up to the wave's longest list cmax rounded up to a multiple of 8.
@@ -923,42 +948,37 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   // per batch, up to the longer wave maximum rounded up to 8.  use(gq, score)
   // in list order.
   auto scan_scores = [&](auto&& use) {
-    const int m = max(cmax[0], cmax[1]);
+    const int m = max_over(cmax);
     for (int e0 = 0; e0 < m; e0 += 8) {
-      f32x4 v0[8], v1[8];
+      f32x4 v[G][8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        v0[u] = *reinterpret_cast<const f32x4*>(slot + entry_idx(e0 + u, 0) * 16u);
-        v1[u] = *reinterpret_cast<const f32x4*>(slot + entry_idx(e0 + u, 1) * 16u);
-      }
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (e0 + u < cc[0]) {
+        for (int gq = 0; gq < G; ++gq) v[gq][u] = *reinterpret_cast<const f32x4*>(slot + entry_idx(e0 + u, gq) * 16u);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) use(0, v0[u][i]);
-        }
-        if (e0 + u < cc[1]) {
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) use(1, v1[u][i]);
-        }
-      }
+        for (int gq = 0; gq < G; ++gq)
+          if (e0 + u < cc[gq]) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) use(gq, v[gq][u][i]);
+          }
     }
   };
   // The compacted singles of both lists for an evaluation (4-byte loads).
   auto scan_scores_compact = [&](auto&& use) {
-    const int m = max(nsmax[0], nsmax[1]);
+    const int m = max_over(nsmax);
     for (int e0 = 0; e0 < m; e0 += 8) {
-      float v0[8], v1[8];
+      float v[G][8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        v0[u] = *reinterpret_cast<const float*>(sslot + entry_idx(e0 + u, 0) * 4u);
-        v1[u] = *reinterpret_cast<const float*>(sslot + entry_idx(e0 + u, 1) * 4u);
-      }
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (e0 + u < ns[0]) use(0, v0[u]);
-        if (e0 + u < ns[1]) use(1, v1[u]);
-      }
+        for (int gq = 0; gq < G; ++gq) v[gq][u] = *reinterpret_cast<const float*>(sslot + entry_idx(e0 + u, gq) * 4u);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq)
+          if (e0 + u < ns[gq]) use(gq, v[gq][u]);
     }
   };
   // The compacted singles of list gq with their key blocks: use(score, kb).
@@ -979,23 +999,23 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   };
   // The quads of both lists with their keys: use(gq, quad, key).
   auto scan_quads_both = [&](auto&& use) {
-    const int m = max(cmax[0], cmax[1]);
+    const int m = max_over(cmax);
     for (int e0 = 0; e0 < m; e0 += 8) {
-      f32x4 v0[8], v1[8];
-      int k0[8], k1[8];
+      f32x4 v[G][8];
+      int kq[G][8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const uint32_t i0 = entry_idx(e0 + u, 0), i1 = entry_idx(e0 + u, 1);
-        v0[u] = *reinterpret_cast<const f32x4*>(slot + i0 * 16u);
-        v1[u] = *reinterpret_cast<const f32x4*>(slot + i1 * 16u);
-        k0[u] = *reinterpret_cast<const uint16_t*>(kslot + i0 * 2u);
-        k1[u] = *reinterpret_cast<const uint16_t*>(kslot + i1 * 2u);
-      }
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (e0 + u < cc[0]) use(0, v0[u], k0[u]);
-        if (e0 + u < cc[1]) use(1, v1[u], k1[u]);
-      }
+        for (int gq = 0; gq < G; ++gq) {
+          const uint32_t idx = entry_idx(e0 + u, gq);
+          v[gq][u] = *reinterpret_cast<const f32x4*>(slot + idx * 16u);
+          kq[gq][u] = *reinterpret_cast<const uint16_t*>(kslot + idx * 2u);
+        }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq)
+          if (e0 + u < cc[gq]) use(gq, v[gq][u], kq[gq][u]);
     }
   };
   // Lists of singles of a later fill: use(score, key).
@@ -1010,19 +1030,18 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     }
   };
   auto scan_scores_singles = [&](auto&& use) {
-    const int m = max(cmax[0], cmax[1]);
+    const int m = max_over(cmax);
     for (int e0 = 0; e0 < m; e0 += 8) {
-      float v0[8], v1[8];
+      float v[G][8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        v0[u] = reinterpret_cast<const CandEntry*>(slot + entry_idx(e0 + u, 0) * 8u)->s;
-        v1[u] = reinterpret_cast<const CandEntry*>(slot + entry_idx(e0 + u, 1) * 8u)->s;
-      }
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (e0 + u < cc[0]) use(0, v0[u]);
-        if (e0 + u < cc[1]) use(1, v1[u]);
-      }
+        for (int gq = 0; gq < G; ++gq) v[gq][u] = reinterpret_cast<const CandEntry*>(slot + entry_idx(e0 + u, gq) * 8u)->s;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq)
+          if (e0 + u < cc[gq]) use(gq, v[gq][u]);
     }
   };
   // Keeps the quads of list gq with a score above `sb` (all lanes of the
@@ -1035,7 +1054,9 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     });
     cc[gq] = k;
   };
-  float sb[2] = {-INFINITY, -INFINITY};  // collection thresholds
+  float sb[G];  // collection thresholds
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq) sb[gq] = -INFINITY;
   __shared__ int fill_dead;              // a list overflowed: stop collecting
   if (threadIdx.x == 0) fill_dead = 0;   // read after the first block's barrier
   // With a cache slot, a first stream over the leading key blocks finds
@@ -1063,14 +1084,14 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       dma_wait();
       __syncthreads();
       if (kb + 1 < w_hi) dma.issue(kbuf[(kb + 1) & 1], K, (kb + 1) * BLK, n);
-      f32x16 s[2][2];
-      int k[2][2];
+      f32x16 s[2][G];
+      int k[2][G];
       const bool valid = block(kb, kbuf[kb & 1], s, k);
       if (valid) {
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
-          for (int gq = 0; gq < 2; ++gq)
+          for (int gq = 0; gq < G; ++gq)
             if (k[h][gq]) tile_max(s[h][gq], gq);
       }
       W = kb + 1;
@@ -1078,7 +1099,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       if (W == w_lo) {
         int above = 0;
 #pragma unroll
-        for (int gq = 0; gq < 2; ++gq) {
+        for (int gq = 0; gq < G; ++gq) {
           float u[8];
           row_top8(gq, u);
           const float b = row_ok[gq] ? score_bound(u, true) : INFINITY;
@@ -1097,7 +1118,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     dma_wait();  // the copy of block W may still be in flight
     __syncthreads();
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq) {
+    for (int gq = 0; gq < G; ++gq) {
       float u[8];
       row_top8(gq, u);
       sb[gq] = row_ok[gq] ? score_bound(u, true) : INFINITY;
@@ -1110,14 +1131,14 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     // once the lists have overflowed, the first stream's blocks need nothing
     // more (their maxima are in)
     if (kb < W && fill_dead) return;
-    f32x16 s[2][2];
-    int k[2][2];
+    f32x16 s[2][G];
+    int k[2][G];
     if (!block(kb, kt, s, k)) return;
-    float tm[2][2], gm[2][2][4];
+    float tm[2][G], gm[2][G][4];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq) {
+      for (int gq = 0; gq < G; ++gq) {
         const float v = quad_maxima(s[h][gq], gm[h][gq]);
         tm[h][gq] = k[h][gq] ? v : -INFINITY;
         if (kb >= W && k[h][gq]) insert_max(v, gq);
@@ -1129,7 +1150,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     // maxima only change from block W on.
     if (kb >= W && (kb & 3) == 0) {
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq) {
+      for (int gq = 0; gq < G; ++gq) {
         float u[8];
         row_top8(gq, u);
         if (row_ok[gq]) sb[gq] = fmaxf(sb[gq], score_bound(u, (kb & 31) == 0));
@@ -1137,7 +1158,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     }
     // a block adds at most 8 quads to each list
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq) {
+    for (int gq = 0; gq < G; ++gq) {
       if (__ballot(cc[gq] > a.cap - 8) != 0ull) {
         filter(gq, sb[gq]);
         if (__ballot(cc[gq] > a.cap - 8) != 0ull) {
@@ -1154,7 +1175,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq)
+      for (int gq = 0; gq < G; ++gq)
         if (__ballot(tm[h][gq] > sb[gq]) != 0ull) {
 #pragma unroll
           for (int r0 = 0; r0 < 16; r0 += 4) {
@@ -1166,9 +1187,9 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         }
   });
 
-  float lo[2], hi[2], tau[2];
+  float lo[G], hi[G], tau[G];
 #pragma unroll
-  for (int gq = 0; gq < 2; ++gq) {
+  for (int gq = 0; gq < G; ++gq) {
     float u[8];
     row_top8(gq, u);
     lo[gq] = hi[gq] = tau[gq] = 0.f;
@@ -1191,20 +1212,22 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
   bool cached = cache && !__syncthreads_or(fill_dead != 0);
   if (cached) {
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq) cmax[gq] = wave_max(cc[gq]);
+    for (int gq = 0; gq < G; ++gq) cmax[gq] = wave_max(cc[gq]);
   }
   int attempts = cache ? 1 : 0;  // cache fills tried (pass 0 is the first)
   // form of the lists: 0 quads, 1 compacted singles, 2 singles of a later fill
   int lists = 0;
   bool fits = false;             // a fill at the current lower end would fit
-  float f_prev[2] = {INFINITY, INFINITY};
+  float f_prev[G];
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq) f_prev[gq] = INFINITY;
 
   for (int it = 0;; ++it) {
     // ---- evaluation at tau (per group): m0 = sum z^gamma, m1 = sum
     // z^(gamma-1), m2 = sum z^(gamma-2) over the strict support z > 0, mc =
     // the size of the support.
-    float m0[2] = {0.f, 0.f}, m1[2] = {0.f, 0.f}, m2[2] = {0.f, 0.f};
-    int mc[2] = {0, 0};
+    float m0[G] = {}, m1[G] = {}, m2[G] = {};
+    int mc[G] = {};
     auto add_z = [&](float zp, int gq) {
       if constexpr (GK == 1) {
         m0[gq] += zp;
@@ -1263,9 +1286,9 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     // Appends the entries x > lo of a sub-tile to list gq; every later tau
     // stays >= lo, so entries left out are 0 there.  The threshold in score
     // units carries a margin for the rounding of lo / c.
-    float s_lo[2];
+    float s_lo[G];
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq) {
+    for (int gq = 0; gq < G; ++gq) {
       const float t0 = lo[gq] / c;
       s_lo[gq] = row_ok[gq] ? t0 - 1e-6f * fmaxf(fabsf(t0), 1.f / c) : INFINITY;
     }
@@ -1282,11 +1305,11 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       }
     };
     auto fill_done = [&]() {
-      if (!__syncthreads_or(cc[0] > scap || cc[1] > scap)) {
+      if (!__syncthreads_or(any_over(cc, scap))) {
         cached = true;
         lists = 2;
-        cmax[0] = wave_max(cc[0]);
-        cmax[1] = wave_max(cc[1]);
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq) cmax[gq] = wave_max(cc[gq]);
       }
     };
 
@@ -1296,15 +1319,16 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     // lower end as it stands now, which has only risen since, so it fits.
     if (!cached && cache && it >= 1 && attempts < 2 && fits) {
       ++attempts;
-      cc[0] = cc[1] = 0;
+#pragma unroll
+      for (int gq = 0; gq < G; ++gq) cc[gq] = 0;
       stream([&](int kb, const E* kt) {
-        f32x16 s[2][2];
-        int k[2][2];
+        f32x16 s[2][G];
+        int k[2][G];
         if (!block(kb, kt, s, k)) return;
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
-          for (int gq = 0; gq < 2; ++gq)
+          for (int gq = 0; gq < G; ++gq)
             if (k[h][gq]) fill_tile(s[h][gq], gq, kb * BLK + 32 * h);
       });
       ++passes;
@@ -1315,17 +1339,22 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       // first one after an overflow also counts the scores above the lower
       // end, the size of a fill at this point.
       const bool count = cache && attempts < 2;
-      int over[2] = {0, 0};
+      int over[G] = {};
+      // with G = 1 two waves share the words of a query block, so they are
+      // cleared here and each wave ORs its bits in (after the stream's first
+      // barrier)
+      if constexpr (G == 1)
+        for (int x = lane; x < TW; x += 64) bits[qbl * BW + x] = 0;
       uint32_t word = 0;  // mask bits of the current 32-block group (wave-uniform)
       stream([&](int kb, const E* kt) {
-        f32x16 s[2][2];
-        int k[2][2];
+        f32x16 s[2][G];
+        int k[2][G];
         bool any = false;
         if (block(kb, kt, s, k)) {
 #pragma unroll
           for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int gq = 0; gq < 2; ++gq)
+            for (int gq = 0; gq < G; ++gq)
               if (k[h][gq]) {
                 any |= eval_tile(s[h][gq], gq);
                 if (count) {
@@ -1336,13 +1365,18 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         }
         if (__ballot(any) != 0ull) word |= 1u << (kb & 31);
         if ((kb & 31) == 31 || kb == nkb - 1) {
-          if (lane == 0) bits[w * BW + (kb >> 5)] = word;
+          if (lane == 0) {
+            if constexpr (G == 2)
+              bits[qbl * BW + (kb >> 5)] = word;
+            else
+              atomicOr(&bits[qbl * BW + (kb >> 5)], word);
+          }
           word = 0;
         }
       });
       ++passes;
       if (count) {
-        fits = !__syncthreads_or(over[0] > scap || over[1] > scap);
+        fits = !__syncthreads_or(any_over(over, scap));
         if (!fits) attempts = 2;  // no retry, and no more counting
       }
     } else if (lists == 2) {
@@ -1357,8 +1391,8 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       // end with the compacted arrays: a score that stays out, or one past
       // the capacity, gets an offset past the end and its stores are
       // dropped (no branches, one increment of the count).
-      int cs[2] = {0, 0};
-      const uint32_t sbytes = (uint32_t)a.cap * 2 * SV_NT * 4;
+      int cs[G] = {};
+      const uint32_t sbytes = (uint32_t)a.cap * G * SV_NT * 4;
       const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(sslot, sbytes), rk = buffer_rsrc(bslot, sbytes / 2);
       scan_quads_both([&](int gq, const f32x4& v, int key4) {
 #pragma unroll
@@ -1374,21 +1408,22 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
           cs[gq] += keep ? 1 : 0;
         }
       });
-      if (!__syncthreads_or(cs[0] > a.cap || cs[1] > a.cap)) {
+      if (!__syncthreads_or(any_over(cs, a.cap))) {
         lists = 1;
-        ns[0] = cs[0];
-        ns[1] = cs[1];
-        nsmax[0] = wave_max(ns[0]);
-        nsmax[1] = wave_max(ns[1]);
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq) {
+          ns[gq] = cs[gq];
+          nsmax[gq] = wave_max(ns[gq]);
+        }
       }
     } else {
       scan_scores([&](int gq, float sv) { add_z(relu_z(c, sv, tau[gq]), gq); });
     }
 
     bool conv = true;
-    float f[2], f1[2], f2[2];
+    float f[G], f1[G], f2[G];
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq) {
+    for (int gq = 0; gq < G; ++gq) {
       if constexpr (GK == 1) m1[gq] = (float)mc[gq];
       if constexpr (GK == 2) m2[gq] = (float)mc[gq];
       m0[gq] = sum_halves(m0[gq]);
@@ -1418,7 +1453,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     evals = it + 1;
     if (stop && !cached) break;
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq) {
+    for (int gq = 0; gq < G; ++gq) {
       if (!row_ok[gq]) continue;
       // the update rules of tau_solve_kernel: B_f (Eq. 4), the Newton lower
       // bound for convex f, H_f (Eq. 5) with the bracket test and slack, and
@@ -1450,10 +1485,10 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     // bracket, widened by the rounding of its fp32 ends.
     const float* Qf = reinterpret_cast<const float*>(Q);
     const float* Kf = reinterpret_cast<const float*>(K);
-    float band[2];
-    double t64[2];
+    float band[G];
+    double t64[G];
 #pragma unroll
-    for (int gq = 0; gq < 2; ++gq) {
+    for (int gq = 0; gq < G; ++gq) {
       band[gq] = PRECISE_BAND * fmaxf(1.f, fabsf(tau[gq]));
       t64[gq] = tau[gq];
     }
@@ -1462,23 +1497,23 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     auto visit = [&](auto&& use) {
       if (cached && lists == 2) {
 #pragma unroll
-        for (int gq = 0; gq < 2; ++gq) scan_singles(gq, [&](float sv, int jv) { use(gq, sv, jv); });
+        for (int gq = 0; gq < G; ++gq) scan_singles(gq, [&](float sv, int jv) { use(gq, sv, jv); });
       } else if (cached) {
 #pragma unroll
-        for (int gq = 0; gq < 2; ++gq)
+        for (int gq = 0; gq < G; ++gq)
           scan_quads(gq, [&](const f32x4& v, int key4) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) use(gq, v[i], 4 * key4 + i);
           });
       } else {
         stream([&](int kb, const E* kt) {
-          f32x16 s[2][2];
-          int k[2][2];
+          f32x16 s[2][G];
+          int k[2][G];
           if (!block(kb, kt, s, k)) return;
 #pragma unroll
           for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int gq = 0; gq < 2; ++gq)
+            for (int gq = 0; gq < G; ++gq)
               if (k[h][gq]) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) use(gq, s[h][gq][r], kb * BLK + 32 * h + crow(r));
@@ -1494,7 +1529,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
       return exact_x<D>(Qf + (size_t)qi[gq] * D, Kf + (size_t)jv * D, a.c64) - t64[gq];
     };
     for (int it = 0; it < 3; ++it) {
-      double s0[2] = {0.0, 0.0}, s1[2] = {0.0, 0.0};
+      double s0[G] = {}, s1[G] = {};
       visit([&](int gq, float sv, int jv) {
         if (!row_ok[gq]) return;
         const double z = z64(gq, sv, jv);
@@ -1504,7 +1539,7 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
         }
       });
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq) {
+      for (int gq = 0; gq < G; ++gq) {
         s0[gq] += __shfl_xor(s0[gq], 32);
         s1[gq] += __shfl_xor(s1[gq], 32);
         if (row_ok[gq] && s1[gq] > 0.0) {
@@ -1516,27 +1551,27 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     }
     if (lane < 32) {
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq)
+      for (int gq = 0; gq < G; ++gq)
         if (row_ok[gq]) {
           const float th = (float)t64[gq];
           a.tau[(size_t)bh * n + qi[gq]] = th;
           a.tau_lo[(size_t)bh * n + qi[gq]] = (float)(t64[gq] - (double)th);
         }
     }
-    for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
+    for (int x = lane; x < TW; x += 64) bits[qbl * BW + x] = 0;
     __syncthreads();
     visit([&](int gq, float sv, int jv) {
       if (!row_ok[gq]) return;
       const float raw = fmaf(c, sv, -tau[gq]);
       if (raw >= band[gq] || z64(gq, sv, jv) > 0.0) {
         const int kv = jv >> 6;
-        atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+        atomicOr(&bits[qbl * BW + (kv >> 5)], 1u << (kv & 31));
       }
     });
   } else {
     if (lane < 32) {
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq)
+      for (int gq = 0; gq < G; ++gq)
         if (row_ok[gq]) {
           a.tau[(size_t)bh * n + qi[gq]] = tau[gq];
           if (std::is_same<E, float>::value) a.tau_lo[(size_t)bh * n + qi[gq]] = 0.f;
@@ -1544,20 +1579,20 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
     }
     if (cached) {
       // mask bits at the returned tau from the cached entries
-      for (int x = lane; x < TW; x += 64) bits[w * BW + x] = 0;
+      for (int x = lane; x < TW; x += 64) bits[qbl * BW + x] = 0;
       __syncthreads();
 #pragma unroll
-      for (int gq = 0; gq < 2; ++gq) {
+      for (int gq = 0; gq < G; ++gq) {
         if (lists == 2) {
           scan_singles(gq, [&](float sv, int jv) {
             const int kv = jv >> 6;
-            if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+            if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[qbl * BW + (kv >> 5)], 1u << (kv & 31));
           });
           continue;
         }
         if (lists == 1) {
           scan_compact(gq, [&](float sv, int kv) {
-            if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+            if (in_support(relu_z(c, sv, tau[gq]))) atomicOr(&bits[qbl * BW + (kv >> 5)], 1u << (kv & 31));
           });
           continue;
         }
@@ -1567,16 +1602,16 @@ __global__ __launch_bounds__(SV_NT, sizeof(E) == 4 && D == 128 ? 1 : 2) void sol
           for (int i = 0; i < 4; ++i) any |= in_support(relu_z(c, v[i], tau[gq])) != 0;
           if (any) {
             const int kv = key4 >> 4;  // key block of the quad
-            atomicOr(&bits[w * BW + (kv >> 5)], 1u << (kv & 31));
+            atomicOr(&bits[qbl * BW + (kv >> 5)], 1u << (kv & 31));
           }
         });
       }
     }
   }
   __syncthreads();
-  if (!wave_ok) return;
+  if (!wave_ok || !writer) return;
   for (int kb = lane; kb < T; kb += 64) {
-    const uint8_t b = (bits[w * BW + (kb >> 5)] >> (kb & 31)) & 1u;
+    const uint8_t b = (bits[qbl * BW + (kb >> 5)] >> (kb & 31)) & 1u;
     a.mask[((size_t)bh * T + qb) * T + kb] = b;
   }
   if (a.stats && lane == 0) {
@@ -1612,13 +1647,24 @@ hipError_t launch_tau_d(const TauArgs& a, hipStream_t s) {
   return launch_tiles(kernel, a, TAU_ROWS, TAU_NT, s);
 }
 
+template <typename E, int D, int G>
+hipError_t launch_solve_g(TauArgs a, hipStream_t s) {
+  auto kernel = solve_kernel<E, D, 0, G>;
+  if (a.gk == 1) kernel = solve_kernel<E, D, 1, G>;
+  if (a.gk == 2) kernel = solve_kernel<E, D, 2, G>;
+  if (a.gk == 4) kernel = solve_kernel<E, D, 4, G>;
+  // a slot of the two-group form holds the lists of two one-group tiles
+  if (G == 1) a.slots *= 2;
+  return launch_tiles(kernel, a, SV_ROWS / 2 * G, SV_NT, s);
+}
+
+// Grids of fewer than two 256-row tiles per compute unit run the one-group
+// form: twice the workgroups, each wave with half the rows.
 template <typename E, int D>
 hipError_t launch_solve_d(const TauArgs& a, hipStream_t s) {
-  auto kernel = solve_kernel<E, D, 0>;
-  if (a.gk == 1) kernel = solve_kernel<E, D, 1>;
-  if (a.gk == 2) kernel = solve_kernel<E, D, 2>;
-  if (a.gk == 4) kernel = solve_kernel<E, D, 4>;
-  return launch_tiles(kernel, a, SV_ROWS, SV_NT, s);
+  const int64_t tiles = (int64_t)a.BH * ((a.n + SV_ROWS - 1) / SV_ROWS);
+  if (tiles < SV_G1_BELOW) return launch_solve_g<E, D, 1>(a, s);
+  return launch_solve_g<E, D, 2>(a, s);
 }
 
 template <int MODE>
