@@ -617,9 +617,11 @@ constexpr int SV_WAVES = SOLVE_THREADS / 64;
 constexpr int SV_NT = SOLVE_THREADS;
 constexpr int SV_ROWS = SOLVE_ROWS;
 // waves per SIMD for the one-group form (G = 1) of solve_kernel, and the
-// grids that use it: fewer 256-row tiles than two per compute unit
+// grids that use it: fewer 256-row tiles than two per compute unit, and at
+// d = 64 rows of up to SV_G1_MAX_N keys
 constexpr int SV_OCC1 = 3;
 constexpr int SV_G1_BELOW = 512;
+constexpr int SV_G1_MAX_N = 32768;
 // threads (of SV_NT) with a score above the running bound in one key block
 // at or below which the solver's first stream ends early
 constexpr int WARM_STOP = SV_NT / 2;
@@ -1658,12 +1660,19 @@ hipError_t launch_solve_g(TauArgs a, hipStream_t s) {
   return launch_tiles(kernel, a, SV_ROWS / 2 * G, SV_NT, s);
 }
 
-// Grids of fewer than two 256-row tiles per compute unit run the one-group
-// form: twice the workgroups, each wave with half the rows.
+// The one-group form has twice the workgroups, each wave with half the rows
+// and three waves per SIMD instead of two, but every K fragment read from
+// LDS feeds one product instead of two and twice as many workgroups stream
+// K.  It runs grids of fewer than two 256-row tiles per compute unit, and at
+// d = 64 (half the fragment reads per product) rows of up to 32768 keys.
+// Measured solver times, one-group against two-group form: B8 H12 n1024 d64
+// 0.122 against 0.160 ms (c = 1); B4 H12 n4096 d64 causal 0.20 against 0.25;
+// B1 H8 d64 causal n = 16384 / 32768 / 65536: 0.27 / 1.14 / 4.50 against
+// 0.42 / 1.21 / 4.04; B1 H16 n8192 d128: 0.75 against 0.62.
 template <typename E, int D>
 hipError_t launch_solve_d(const TauArgs& a, hipStream_t s) {
   const int64_t tiles = (int64_t)a.BH * ((a.n + SV_ROWS - 1) / SV_ROWS);
-  if (tiles < SV_G1_BELOW) return launch_solve_g<E, D, 1>(a, s);
+  if (tiles < SV_G1_BELOW || (D <= 64 && a.n <= SV_G1_MAX_N)) return launch_solve_g<E, D, 1>(a, s);
   return launch_solve_g<E, D, 2>(a, s);
 }
 
