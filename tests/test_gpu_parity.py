@@ -67,6 +67,17 @@ def test_small_shapes(dtype, n, causal, d):
                    label="small-%s-a%g" % (dtype, alpha))
 
 
+@pytest.mark.parametrize("alpha", [1.5, 1.7])
+@pytest.mark.parametrize("causal", [False, True])
+def test_f32_two_group_form(alpha, causal):
+    """fp32 at a grid of 512 tiles of 256 rows (B2 H16 n4096 d128), which runs
+    the two-group form of the solver, fwd+bwd on two whole heads: alpha 1.7
+    takes the fp64 refinement of tau (tau + tau_lo) and x - tau in fp64 near
+    the support edge in that form too."""
+    _full_case(2, 16, 4096, 128, "f32", alpha, causal, True, 2.0, 300, heads=[0, 31],
+               label="f32-g2-a%g" % alpha)
+
+
 @pytest.mark.parametrize("c", [1.0, 4.0, 16.0])
 def test_encoder_forward(c):
     """B8 H12 n1024 d64 bf16 forward, Q temperature c; 4 heads vs the oracle."""
