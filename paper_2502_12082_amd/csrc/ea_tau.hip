@@ -625,6 +625,8 @@ constexpr int SV_G1_MAX_N = 32768;
 // threads (of SV_NT) with a score above the running bound in one key block
 // at or below which the solver's first stream ends early
 constexpr int WARM_STOP = SV_NT / 2;
+// above it, at d = 64, the first stream covers every key block
+constexpr int WARM_ALL = 3 * SV_NT / 4;
 static_assert(SV_ROWS == 64 * SV_WAVES, "one 64-row query block per wave (G = 2)");
 
 // G = 2: each wave owns one 64-row query block as two groups of 32 rows.
@@ -1066,21 +1068,24 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
   // close to its final value instead of collecting (and later dropping) most
   // scores of its first blocks.  Those blocks' maxima are then not inserted
   // again (the bound needs distinct keys).  The stream covers an eighth of
-  // the key blocks, or else half of them (all of them at d = 64, where a
-  // block's products cost half as much against the collection work they
-  // save: the encoder shape, n = 1024, took 0.147 against 0.183 ms).  After
-  // the eighth it counts the threads holding
-  // a score of the last block above the bound of the maxima so far, and
-  // stops there if at most WARM_STOP of them do: for rows with few large
-  // scores the collection is cheap and a longer stream only adds MFMA work,
-  // for rows with many it saves list stores.  (Measured at n = 8192 with a
+  // the key blocks, half of them, or all of them.  After the eighth it
+  // counts the threads holding a score of the last block above the bound of
+  // the maxima so far, and stops there if at most WARM_STOP of them do: for
+  // rows with few large scores the collection is cheap and a longer stream
+  // only adds MFMA work, for rows with many it saves list stores.  At d = 64,
+  // where a block's products cost half as much against the collection work
+  // they save, more than WARM_ALL such threads take the stream over every
+  // block (B8 H12 n1024 c = 1: 0.120 against 0.153 ms; where fewer pass,
+  // half was faster, e.g. B4 H12 n4096 causal c = 8 0.195 against 0.213 ms
+  // for every block).  (Measured at n = 8192 with a
   // fixed length: an eighth, a quarter and a half of the blocks cost 0.77 /
   // 0.75 / 0.73 ms at c = 1, while at c = 16 and at n = 65536 causal the
   // eighth was the fastest.  The count after an eighth is 189 of 256
   // threads at c = 1, 95 at c = 2, 49 at c = 4 and 23 at c = 16.)
   int W = 0;
   if (cache) {
-    const int w_lo = max(1, nkb / 8), w_hi = D <= 64 ? nkb : max(1, nkb / 2);
+    const int w_lo = max(1, nkb / 8);
+    int w_hi = max(1, nkb / 2);
     dma.issue(kbuf[0], K, 0, n);
     for (int kb = 0;; ++kb) {
       dma_wait();
@@ -1114,7 +1119,9 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
               }
           }
         }
-        if (__syncthreads_count(above > 0) <= WARM_STOP) break;
+        const int cnt = __syncthreads_count(above > 0);
+        if (cnt <= WARM_STOP) break;
+        if (D <= 64 && cnt > WARM_ALL) w_hi = nkb;
       }
     }
     dma_wait();  // the copy of block W may still be in flight
