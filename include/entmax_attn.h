@@ -117,11 +117,13 @@ ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_s
  *   o        [BH, n, d] in shape->dtype, 16-byte aligned (written)
  *   res      residual buffers (written), 4-byte aligned, o2 16-byte aligned
  *   workspace optional, 16-byte aligned: the solver's candidate cache, in
- *            768 KiB slots.  sizes.ws_fwd holds min(tiles, 512) slots (a
+ *            1.125 MiB slots.  sizes.ws_fwd holds min(tiles, 512) slots (a
  *            tile is 256 query rows of one head), so it does not grow with
- *            B * H * n beyond 384 MiB.  With S slots and more tiles than
+ *            B * H * n beyond 576 MiB.  With S slots and more tiles than
  *            slots the solver runs the tiles in launches of S workgroups,
- *            one slot each.  A tile stores, while it finds the row maxima, the
+ *            one slot each (2 S workgroups of 128 rows, half a slot each, in
+ *            the one-group form the solver takes for small grids and at
+ *            d = 64 for n <= 32768).  A tile stores, while it finds the row maxima, the
  *            scores above each row's lower bracket end and runs its
  *            evaluations on them instead of streaming K again (when the
  *            stored scores do not fit, it streams K, and collects once more
@@ -129,8 +131,8 @@ ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_s
  *            the lower end).  Without a workspace (NULL, or too small for
  *            one slot) every tile streams K on every pass.  Results agree up
  *            to rounding either way.  Contents are scratch.
- * Launches 3 kernels on `stream` (the solver one more per S tiles beyond
- * the first S).
+ * Launches 3 kernels on `stream` (the solver one more per S workgroups
+ * beyond the first S).
  */
 ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const void* q,
                           const void* k, const void* v, void* o, const ea_residuals* res,
