@@ -928,10 +928,34 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
     for (int gq = 0; gq < G; ++gq) r |= v[gq] > limit;
     return r;
   };
+  // Loads of list entries through buffer resources over the slot's arrays:
+  // a lane past its own count gets an offset past the end of the resource,
+  // so that nothing is fetched for it (the value, 0, is never used).  The
+  // scans below run the wave's longest list, so this saves the reads of
+  // the shorter ones.
+  const uint32_t qbytes = (uint32_t)a.cap * G * SV_NT * 16;
+  const __amdgpu_buffer_rsrc_t rq = buffer_rsrc(slot, qbytes), rkq = buffer_rsrc(kslot, qbytes / 8),
+                               rsc = buffer_rsrc(sslot, qbytes / 4), rbk = buffer_rsrc(bslot, qbytes / 8),
+                               rfl = buffer_rsrc(slot, (uint32_t)scap * G * SV_NT * 8);
+  auto off_if = [&](bool ok, int e, int gq, uint32_t size) { return ok ? entry_idx(e, gq) * size : BUFFER_OOB; };
+  auto ld_quad = [&](int e, int gq, bool ok) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, off_if(ok, e, gq, 16u), 0, 0));
+  };
+  auto ld_qkey = [&](int e, int gq, bool ok) {
+    return (int)__builtin_amdgcn_raw_buffer_load_b16(rkq, off_if(ok, e, gq, 2u), 0, 0);
+  };
+  auto ld_single = [&](int e, int gq, bool ok) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsc, off_if(ok, e, gq, 4u), 0, 0));
+  };
+  auto ld_block = [&](int e, int gq, bool ok) {
+    return (int)__builtin_amdgcn_raw_buffer_load_b16(rbk, off_if(ok, e, gq, 2u), 0, 0);
+  };
+  auto ld_fill = [&](int e, int gq, bool ok) {
+    return __builtin_bit_cast(CandEntry, __builtin_amdgcn_raw_buffer_load_b64(rfl, off_if(ok, e, gq, 8u), 0, 0));
+  };
   // Reads list gq of this thread in batches of eight independent quad
-  // loads, up to the wave's longest list cmax rounded up to a multiple of 8.
-  // That stays inside the slot (cmax <= cap, and cap is a multiple of 8);
-  // quads past this thread's own count are stale and never used.
+  // loads, up to the wave's longest list cmax rounded up to a multiple of 8
+  // (inside the slot: cmax <= cap, and cap is a multiple of 8).
   // use(quad, key) for each quad of list gq.
   auto scan_quads = [&](int gq, auto&& use) {
     for (int e0 = 0; e0 < cmax[gq]; e0 += 8) {
@@ -939,9 +963,9 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
       int kv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const uint32_t idx = entry_idx(e0 + u, gq);
-        qv[u] = *reinterpret_cast<const f32x4*>(slot + idx * 16u);
-        kv[u] = *reinterpret_cast<const uint16_t*>(kslot + idx * 2u);
+        const bool ok = e0 + u < cc[gq];
+        qv[u] = ld_quad(e0 + u, gq, ok);
+        kv[u] = ld_qkey(e0 + u, gq, ok);
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u)
@@ -958,7 +982,7 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
-        for (int gq = 0; gq < G; ++gq) v[gq][u] = *reinterpret_cast<const f32x4*>(slot + entry_idx(e0 + u, gq) * 16u);
+        for (int gq = 0; gq < G; ++gq) v[gq][u] = ld_quad(e0 + u, gq, e0 + u < cc[gq]);
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
@@ -977,7 +1001,7 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
-        for (int gq = 0; gq < G; ++gq) v[gq][u] = *reinterpret_cast<const float*>(sslot + entry_idx(e0 + u, gq) * 4u);
+        for (int gq = 0; gq < G; ++gq) v[gq][u] = ld_single(e0 + u, gq, e0 + u < ns[gq]);
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
@@ -992,9 +1016,9 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
       int kv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const uint32_t idx = entry_idx(e0 + u, gq);
-        v[u] = *reinterpret_cast<const float*>(sslot + idx * 4u);
-        kv[u] = *reinterpret_cast<const uint16_t*>(bslot + idx * 2u);
+        const bool ok = e0 + u < ns[gq];
+        v[u] = ld_single(e0 + u, gq, ok);
+        kv[u] = ld_block(e0 + u, gq, ok);
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u)
@@ -1011,9 +1035,9 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
       for (int u = 0; u < 8; ++u)
 #pragma unroll
         for (int gq = 0; gq < G; ++gq) {
-          const uint32_t idx = entry_idx(e0 + u, gq);
-          v[gq][u] = *reinterpret_cast<const f32x4*>(slot + idx * 16u);
-          kq[gq][u] = *reinterpret_cast<const uint16_t*>(kslot + idx * 2u);
+          const bool ok = e0 + u < cc[gq];
+          v[gq][u] = ld_quad(e0 + u, gq, ok);
+          kq[gq][u] = ld_qkey(e0 + u, gq, ok);
         }
 #pragma unroll
       for (int u = 0; u < 8; ++u)
@@ -1027,7 +1051,7 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
     for (int e0 = 0; e0 < cmax[gq]; e0 += 8) {
       CandEntry ce[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) ce[u] = *reinterpret_cast<const CandEntry*>(slot + entry_idx(e0 + u, gq) * 8u);
+      for (int u = 0; u < 8; ++u) ce[u] = ld_fill(e0 + u, gq, e0 + u < cc[gq]);
 #pragma unroll
       for (int u = 0; u < 8; ++u)
         if (e0 + u < cc[gq]) use(ce[u].s, ce[u].j);
@@ -1040,7 +1064,7 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
-        for (int gq = 0; gq < G; ++gq) v[gq][u] = reinterpret_cast<const CandEntry*>(slot + entry_idx(e0 + u, gq) * 8u)->s;
+        for (int gq = 0; gq < G; ++gq) v[gq][u] = ld_fill(e0 + u, gq, e0 + u < cc[gq]).s;
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
