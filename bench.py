@@ -5,8 +5,9 @@
 Workload (the sparsity-sweep shape): batch 1, 16 heads, n = 8192, d = 128,
 bf16 inputs, non-causal, alpha = 1.5, scale = 1/sqrt(d); Q ~ c N(0,1),
 K, V, dO ~ N(0,1), seeded synthetic data.  One step = the whole path: tau
-solver, table compaction, sparse forward (with O2), delta, dK/dV, dQ, each
-launched through the C ABI stage entry points on the current stream.
+solver (with the mask's row tables), sparse forward (with O2 and the column
+tables), delta, dK/dV, dQ, each launched through the C ABI stage entry points
+on the current stream.
 
 Prints ONE JSON line.  `value` is dense-equivalent TFLOP/s (14 n^2 d per head
 for forward + backward, the FlashAttention convention) at the headline
@@ -32,7 +33,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "fwd+bwd ms & effective TFLOP/s vs sparsity, n=8192 d=128 α=1.5 (1 GPU)"
 PEAK_BF16_TFLOPS = 2500.0
-KERNELS = ("tau_solve", "compact", "fwd_sparse", "bwd_delta", "bwd_dkdv", "bwd_dq")
+KERNELS = ("tau_solve", "fwd_sparse", "bwd_delta", "bwd_dkdv", "bwd_dq")
 # MFMA block products (64 x 64 x d each) per listed block, by kernel
 PRODUCTS_PER_ACTIVE = {"fwd_sparse": 3, "bwd_dkdv": 4, "bwd_dq": 3}
 # kernel name fragment in profiler output, and the sources that define each kernel
@@ -305,7 +306,7 @@ class Runner:
         self.ws = torch.empty(self.res.sizes.ws_bwd // 4 + 4, dtype=torch.float32,
                               device=self.q.device)
         self.ws_fwd = ea.forward_workspace(self.res, self.q.device)
-        self.events = [[torch.cuda.Event(enable_timing=True) for _ in range(7)]
+        self.events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(KERNELS) + 1)]
                        for _ in range(max(1, args.steps))]
 
     def step(self, ev=None):
@@ -313,7 +314,7 @@ class Runner:
         q, k, v, do = self.q.data_ptr(), self.k.data_ptr(), self.v.data_ptr(), self.do.data_ptr()
         if ev:
             ev[0].record()
-        for st in range(3):
+        for st in range(2):
             ea._check(ea.entmax_attn_fwd_stage(st, self.shape, self.params, q, k, v,
                                                self.o.data_ptr(), self.rp, self.ws_fwd.data_ptr(),
                                                self.ws_fwd.numel(), s), "fwd stage")
@@ -327,7 +328,7 @@ class Runner:
                                                self.dv.data_ptr(), self.ws.data_ptr(),
                                                self.ws.numel() * 4, s), "bwd stage")
             if ev:
-                ev[4 + st].record()
+                ev[3 + st].record()
 
     def timed(self, steps, warmup, per_kernel=True):
         torch = self.torch
@@ -379,7 +380,7 @@ class Runner:
         # key blocks that precedes a candidate collection is an implementation
         # choice, not work of the method, and is left out.
         solver_blocks = float((stats * per_qb[None, :]).sum())
-        flops = {"tau_solve": solver_blocks * f_blk, "compact": 0.0, "bwd_delta": 0.0}
+        flops = {"tau_solve": solver_blocks * f_blk, "bwd_delta": 0.0}
         for k_, m in PRODUCTS_PER_ACTIVE.items():
             # the forward without a backward to follow forms S and P V only
             if k_ == "fwd_sparse" and not self.bwd:

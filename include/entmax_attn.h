@@ -131,7 +131,7 @@ ea_status entmax_attn_sizes(const ea_shape* shape, const ea_params* params, ea_s
  *            the lower end).  Without a workspace (NULL, or too small for
  *            one slot) every tile streams K on every pass.  Results agree up
  *            to rounding either way.  Contents are scratch.
- * Launches 3 kernels on `stream` (the solver one more per S workgroups
+ * Launches 2 kernels on `stream` (the solver one more per S workgroups
  * beyond the first S).
  */
 ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const void* q,
@@ -152,16 +152,18 @@ ea_status entmax_attn_bwd(const ea_shape* shape, const ea_params* params, const 
 
 /*
  * The same passes one kernel launch at a time, for callers that schedule or
- * time the stages themselves; entmax_attn_fwd / entmax_attn_bwd are exactly
- * stages 0, 1, 2 in order, with the same argument rules.
- *   forward  stage 0: tau, block_mask and stats (solver, Algorithm 1/3, Eq. 8)
- *            stage 1: q_count/q_index/k_count/k_index from block_mask (Sec. 3.2.1)
- *            stage 2: O (and o2 if need_bwd) from tau and the tables (Algorithm 2, App. A.5)
+ * time the stages themselves; entmax_attn_fwd is exactly stages 0, 1 and
+ * entmax_attn_bwd stages 0, 1, 2, in order, with the same argument rules.
+ *   forward  stage 0: tau, block_mask, q_count/q_index and stats (solver,
+ *                     Algorithm 1/3, Eq. 8; row tables, Sec. 3.2.1)
+ *            stage 1: O (and o2 if need_bwd) from tau and the row tables
+ *                     (Algorithm 2, App. A.5), and k_count/k_index from
+ *                     block_mask (Sec. 3.2.1)
  *   backward stage 0: delta = rowsum(dO * o2) into the workspace (App. A.2)
  *            stage 1: dK, dV over each key block's list (Algorithm 4, Eq. 12-13)
  *            stage 2: dQ over each query block's list (Algorithm 5, Eq. 11)
  * A stage reads what the earlier stages of the same pass wrote.  stage outside
- * 0..2 returns EA_ERR_INVALID_ARG.
+ * 0..1 (forward) or 0..2 (backward) returns EA_ERR_INVALID_ARG.
  */
 ea_status entmax_attn_fwd_stage(int stage, const ea_shape* shape, const ea_params* params,
                                 const void* q, const void* k, const void* v, void* o,

@@ -1,6 +1,6 @@
 // ea_api.hip -- the C ABI: argument checks, buffer sizes and the launch
-// sequence of the forward (tau solver -> table compaction -> sparse forward)
-// and backward (delta -> dK/dV -> dQ) passes.
+// sequence of the forward (tau solver with the mask's row tables -> sparse
+// forward with the column tables) and backward (delta -> dK/dV -> dQ) passes.
 #include <math.h>
 #include <stdint.h>
 
@@ -256,17 +256,14 @@ ea_status run_fwd_stage(int stage, const Dims& d, const ea_params* params, const
                SOLVE_QUAD_CAP, (int)slots, /*tile0=*/0,
                (int)d.BH, (int)d.n, (int)d.T, c, params->alpha, gamma, params->causal,
                params->max_iter, params->tol, gk,
-               const_cast<float*>(tau_lo_of(res, d)), c64_of(params), g64_of(params)};
+               const_cast<float*>(tau_lo_of(res, d)), c64_of(params), g64_of(params),
+               res->q_count, res->q_index};
     return from_hip(launch_tau(ta, d.dtype, (int)d.d, s));
-  }
-  if (stage == 1) {
-    CompactArgs ca{res->block_mask, res->q_count, res->q_index, res->k_count, res->k_index,
-                   (int)d.BH, (int)d.T};
-    return from_hip(launch_compact(ca, s));
   }
   FwdArgs fa{q, k, v, o, params->need_bwd ? res->o2 : nullptr, res->tau, res->q_count,
              res->q_index, (int)d.BH, (int)d.n, (int)d.T, c, gamma, params->causal, gk,
-             tau_lo_of(res, d), c64_of(params), g64_of(params)};
+             tau_lo_of(res, d), c64_of(params), g64_of(params),
+             res->block_mask, res->k_count, res->k_index};
   return from_hip(launch_fwd(fa, d.dtype, (int)d.d, params->need_bwd != 0, s));
 }
 
@@ -321,7 +318,7 @@ ea_status entmax_attn_fwd(const ea_shape* shape, const ea_params* params, const 
   ea_status st = prep_fwd(shape, params, q, k, v, o, res, workspace, &d);
   if (st != EA_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  for (int stage = 0; stage < 3; ++stage)
+  for (int stage = 0; stage < 2; ++stage)
     if ((st = run_fwd_stage(stage, d, params, q, k, v, o, res, workspace, ws_bytes, s)) != EA_OK)
       return st;
   return EA_OK;
@@ -331,7 +328,7 @@ ea_status entmax_attn_fwd_stage(int stage, const ea_shape* shape, const ea_param
                                 const void* q, const void* k, const void* v, void* o,
                                 const ea_residuals* res, void* workspace, size_t ws_bytes,
                                 void* stream) {
-  if (stage < 0 || stage > 2) return EA_ERR_INVALID_ARG;
+  if (stage < 0 || stage > 1) return EA_ERR_INVALID_ARG;
   Dims d;
   ea_status st = prep_fwd(shape, params, q, k, v, o, res, workspace, &d);
   if (st != EA_OK) return st;

@@ -1,9 +1,11 @@
-// ea_fwd.hip -- block-mask compaction and the sparse alpha-entmax forward.
+// ea_fwd.hip -- the sparse alpha-entmax forward, and the column tables.
 //
-// Compaction (Sec. 3.2.1, "pointer-increment lookup tables"; App. A.5): from
-// the block mask M, Q_i = {j : M_ij = 1} for every query block i and
-// K_j = {i : M_ij = 1} for every key block j, each list ascending.  Stored as
-// a count per block plus a fixed-stride index row of T entries.
+// Tables (Sec. 3.2.1, "pointer-increment lookup tables"; App. A.5): from the
+// block mask M, Q_i = {j : M_ij = 1} for every query block i and
+// K_j = {i : M_ij = 1} for every key block j, each list ascending, stored as
+// a count per block plus a fixed-stride index row of T entries.  The solver
+// writes Q_i with its mask row; K_j needs every row of the mask, so extra
+// workgroups of the forward's launch build it (the backward reads it).
 //
 // Forward (Algorithm 2 with the masked loop of App. A.5): for every query
 // block i and every key block j in Q_i, recompute S = Q_i K_j^T, P =
@@ -37,45 +39,47 @@ namespace ea {
 
 namespace {
 
-// ------------------------------------------------------------ compaction
+// --------------------------------------------------------------- tables
 
-constexpr int CMP_NT = 256;
-
-__global__ __launch_bounds__(CMP_NT) void compact_kernel(CompactArgs a) {
-  const int lane = lane_id();
-  const long long gw = (long long)blockIdx.x * (CMP_NT / 64) + wave_id();
-  const long long rows = (long long)a.BH * a.T;
-  if (gw >= 2 * rows) return;
-  const bool by_col = gw >= rows;
-  const long long idx = by_col ? gw - rows : gw;
-  const int bh = (int)(idx / a.T), r = (int)(idx % a.T);
-  const int T = a.T;
+// K_j of key block `col` (= bh * T + j), one wave: a ballot and a prefix
+// count per 64 query blocks of the mask's column j.
+__device__ void column_table(const FwdArgs& a, int col) {
+  const int lane = lane_id(), T = a.T;
+  const int bh = col / T, j = col % T;
   const uint8_t* M = a.mask + (size_t)bh * T * T;
-  int32_t* out = (by_col ? a.k_index : a.q_index) + ((size_t)bh * T + r) * T;
-  int base = 0;
-  for (int c0 = 0; c0 < T; c0 += 64) {
-    const int cidx = c0 + lane;
-    bool bit = false;
-    if (cidx < T) bit = (by_col ? M[(size_t)cidx * T + r] : M[(size_t)r * T + cidx]) != 0;
-    const unsigned long long b = __ballot(bit);
-    const int pre = __builtin_amdgcn_mbcnt_hi((unsigned)(b >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)b, 0u));
-    if (bit) out[base + pre] = cidx;
-    base += __popcll(b);
+  int32_t* const out = a.k_index + (size_t)col * T;
+  int listed = 0;
+  for (int i0 = 0; i0 < T; i0 += 64) {
+    const int i = i0 + lane;
+    const bool b = i < T && M[(size_t)i * T + j] != 0;
+    const unsigned long long m = __ballot(b);
+    if (b) out[listed + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u))] = i;
+    listed += __popcll(m);
   }
-  if (lane == 0) (by_col ? a.k_count : a.q_count)[(size_t)bh * T + r] = base;
+  if (lane == 0) a.k_count[col] = listed;
 }
 
 // --------------------------------------------------------------- forward
 
 constexpr int FWD_NT = 256;
+constexpr int FWD_COLS_PER_WG = FWD_NT / 64;  // column tables per extra workgroup
 
 // One 64-row query block per workgroup of 4 waves: wave w takes query half
 // qh = w % 2 and, of every listed key block, key half kh = w / 2.  Each wave
 // accumulates partial O (and U V, sum U) over its key halves; the two
 // partials of a query half are summed through LDS at the end.  The smaller
 // per-wave state lets two waves share each SIMD.
+//
+// Workgroups past the BH * T query blocks build the column tables instead,
+// one key block per wave (they come last in the grid).
 template <typename E, int D, int GK, bool TRAIN>
 __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
+  const int nqb = a.BH * a.T;
+  if ((int)blockIdx.x >= nqb) {
+    const int col = ((int)blockIdx.x - nqb) * FWD_COLS_PER_WG + wave_id();
+    if (col < nqb) column_table(a, col);
+    return;
+  }
   using TL = Tile<E, D>;
   using M = Mma<E>;
   constexpr int KS = D / M::KW;
@@ -254,7 +258,8 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
 
 template <typename E, int D, bool TRAIN>
 hipError_t launch_fwd_dt(const FwdArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)(a.BH * a.T)), block(FWD_NT);
+  const int nqb = a.BH * a.T;
+  dim3 grid((unsigned)(nqb + (nqb + FWD_COLS_PER_WG - 1) / FWD_COLS_PER_WG)), block(FWD_NT);
   auto kernel = fwd_kernel<E, D, 0, TRAIN>;
   if (a.gk == 1) kernel = fwd_kernel<E, D, 1, TRAIN>;
   if (a.gk == 2) kernel = fwd_kernel<E, D, 2, TRAIN>;
@@ -268,12 +273,6 @@ hipError_t launch_fwd_d(const FwdArgs& a, bool train, hipStream_t s) {
 }
 
 }  // namespace
-
-hipError_t launch_compact(const CompactArgs& a, hipStream_t s) {
-  const long long waves = 2LL * a.BH * a.T;
-  dim3 grid((unsigned)((waves + CMP_NT / 64 - 1) / (CMP_NT / 64))), block(CMP_NT);
-  return launch_kernel(compact_kernel, grid, block, s, a);
-}
 
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int head_dim, bool train, hipStream_t s) {
   if (dtype == 0)

@@ -72,12 +72,10 @@ struct TauArgs {
   // in fp64 from the same fp32 parameters
   float* tau_lo;
   double c64, g64;
-};
-
-struct CompactArgs {
-  const uint8_t* mask;
-  int32_t *q_count, *q_index, *k_count, *k_index;
-  int BH, T;
+  // masked path: the row tables of the mask (Q_i of every query block),
+  // written with it
+  int32_t* q_count;   // [BH, T]
+  int32_t* q_index;   // [BH, T, T]
 };
 
 struct FwdArgs {
@@ -95,6 +93,11 @@ struct FwdArgs {
   int gk;
   const float* tau_lo;  // fp32 inputs, general alpha: low part of tau (or null: 0)
   double c64, g64;
+  // the column tables (K_j of every key block), built by extra workgroups of
+  // the same launch from the mask
+  const uint8_t* mask;  // [BH, T, T]
+  int32_t* k_count;     // [BH, T]
+  int32_t* k_index;     // [BH, T, T]
 };
 
 struct BwdArgs {
@@ -154,7 +157,6 @@ inline hipError_t launch_kernel(void (*kernel)(A), dim3 grid, dim3 block, hipStr
 hipError_t launch_tau(const TauArgs& a, int dtype, int head_dim, hipStream_t s);
 // The no-mask forward: tau, then O (and O2 if a.o2) in the same kernel.
 hipError_t launch_tau_fused(const TauArgs& a, int dtype, int head_dim, hipStream_t s);
-hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int head_dim, bool train, hipStream_t s);
 hipError_t launch_delta(const DeltaArgs& a, int dtype, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dkdv(const BwdArgs& a, int dtype, int head_dim, hipStream_t s);

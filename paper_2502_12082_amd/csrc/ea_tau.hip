@@ -1643,10 +1643,19 @@ __global__ __launch_bounds__(SV_NT, G == 1 ? SV_OCC1 : (sizeof(E) == 4 && D == 1
   }
   __syncthreads();
   if (!wave_ok || !writer) return;
-  for (int kb = lane; kb < T; kb += 64) {
-    const uint8_t b = (bits[qbl * BW + (kb >> 5)] >> (kb & 31)) & 1u;
-    a.mask[((size_t)bh * T + qb) * T + kb] = b;
+  // The block's mask row and its row table (Sec. 3.2.1): Q_i ascending, by
+  // a ballot and a prefix count per 64 key blocks.
+  int32_t* const row = a.q_index + ((size_t)bh * T + qb) * T;
+  int listed = 0;
+  for (int k0 = 0; k0 < T; k0 += 64) {
+    const int kb = k0 + lane;
+    const bool b = kb < T && ((bits[qbl * BW + (kb >> 5)] >> (kb & 31)) & 1u);
+    if (kb < T) a.mask[((size_t)bh * T + qb) * T + kb] = b ? 1 : 0;
+    const unsigned long long m = __ballot(b);
+    if (b) row[listed + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u))] = kb;
+    listed += __popcll(m);
   }
+  if (lane == 0) a.q_count[(size_t)bh * T + qb] = listed;
   if (a.stats && lane == 0) {
     a.stats[(size_t)bh * T + qb] = passes;
     a.stats[((size_t)a.BH + bh) * T + qb] = evals;
