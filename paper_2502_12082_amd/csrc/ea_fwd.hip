@@ -116,6 +116,23 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) qf[kk] = load_row_frag_global<E, D>(Q, i, n, kk);
 
+  // At d = 64 a wave raises its issue priority over its MFMA chains, so
+  // that the two waves of a SIMD drift apart (one in its MFMAs while the
+  // other maps scores to P and U) instead of contending in the same phase:
+  // the kernel took 0.070 against 0.082 ms on B8 H12 n1024, 0.220 against
+  // 0.252 on B4 H12 n4096 causal and 0.291 against 0.318 on B1 H8 n16384
+  // causal.  At d = 128 it made no difference (1.03 ms on B1 H16 n8192), and
+  // in the backward kernels it was neutral or slower (dK/dV 1.31 against
+  // 1.27 ms at d = 128), so they do without.
+  auto mfma_priority = [](bool high) {
+    if constexpr (D == 64) {
+      if (high)
+        __builtin_amdgcn_s_setprio(1);
+      else
+        __builtin_amdgcn_s_setprio(0);
+    }
+  };
+
   const int32_t* list = a.q_index + ((size_t)bh * T + qb) * T;
   const int cnt = a.q_count[(size_t)bh * T + qb];
 
@@ -153,8 +170,10 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
     if (kind == 0) continue;
     // S^T = K Q^T for this wave's 32 keys x 32 queries
     f32x16 s = zero16();
+    mfma_priority(true);
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) s = M::mma(lds_row_frag<E, D>(kt, 32 * kh + (lane & 31), kk), qf[kk], s);
+    mfma_priority(false);
     if (kind == 2) {  // invalid keys -> -inf, so [x - tau]_+ is exactly 0 there
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -180,6 +199,7 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
         p[r] = Gamma<GK>::p_only(zp, g);
       }
     }
+    mfma_priority(true);
 #pragma unroll
     for (int t = 0; t < PS; ++t) {
       typename M::frag ph, pl, uh, ul;
@@ -196,6 +216,7 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
         }
       }
     }
+    mfma_priority(false);
   }
 
   // Sum the two key-half partials of each query half through LDS: first O
