@@ -330,11 +330,19 @@ class Runner:
             if ev:
                 ev[3 + st].record()
 
-    def timed(self, steps, warmup, per_kernel=True):
+    def timed(self, steps, warmup, per_kernel=True, warm_s=0.0):
+        """Mean ms per step over `steps` steps after `warmup` untimed ones,
+        followed by more untimed steps until `warm_s` seconds have passed
+        (sub-millisecond steps: the GPU's clocks ramp up over tens of ms)."""
         torch = self.torch
         for _ in range(warmup):
             self.step()
         torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < warm_s:
+            for _ in range(5):
+                self.step()
+            torch.cuda.synchronize()
         t_start = torch.cuda.Event(enable_timing=True)
         t_end = torch.cuda.Event(enable_timing=True)
         wall0 = time.perf_counter()
@@ -523,10 +531,12 @@ def sweep_point(args, alpha, c):
     return out
 
 
-def other_configs(args, steps=5):
+def other_configs(args, steps=20, warmup=5):
     """The other workload shapes, each at its own size: the tiny fp32 forward,
     the encoder-shaped forward at three temperatures and the decoder-shaped
-    training step (ms per call and dense-equivalent TFLOP/s)."""
+    training step (ms per call and dense-equivalent TFLOP/s).  Each call takes
+    0.07-1 ms: 20 timed calls follow at least 50 ms of untimed ones, so that
+    the timed region sees the clocks of a busy GPU."""
     import torch
     cases = [("tiny forward", 1, 1, 256, 64, "f32", False, 1.0, False),
              ("encoder forward", 8, 12, 1024, 64, "bf16", False, 1.0, False),
@@ -538,7 +548,7 @@ def other_configs(args, steps=5):
         a = argparse.Namespace(**{**vars(args), "batch": B, "heads": H, "seqlen": n,
                                   "head_dim": d, "alpha": 1.5, "causal": causal, "steps": steps})
         r = Runner(a, c, dtype=dt, bwd=bwd)
-        ms, _, _ = r.timed(steps, 2, per_kernel=False)
+        ms, _, _ = r.timed(steps, warmup, per_kernel=False, warm_s=0.05)
         w = r.work()
         flops = (14.0 if bwd else 4.0) * n * n * d * B * H * (0.5 if causal else 1.0)
         executed = sum(v_ for k_, v_ in w["flops"].items()

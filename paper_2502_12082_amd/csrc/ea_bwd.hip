@@ -500,7 +500,11 @@ constexpr int DQ_NT = 256;
 // qh = w % 2 and, of every listed key block, key half kh = w / 2, so each
 // wave holds only its 32 query rows and one partial dQ; the two key-half
 // partials are summed through LDS at the end.  Halving the per-wave state
-// lets two waves share each SIMD.
+// lets two waves share each SIMD.  At d = 128 a wave raises its issue
+// priority over its dQ products, so that the two waves of a SIMD drift
+// apart (0.905 against 0.922 ms on B1 H16 n8192 at c = 1, 0.505 against
+// 0.531 at c = 16); at d = 64 that was slower (0.256 against 0.252 ms on
+// B1 H8 n16384 causal).
 template <typename E, int D, int GK>
 __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
   using TL = Tile<E, D>;
@@ -606,6 +610,7 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
       Gamma<GK>::pu(zp, g, p, u);
       dsv[r] = u * (dp[r] - del);
     }
+    if constexpr (D == 128) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int t = 0; t < PS; ++t) {
       typename M::frag dh, dl;
@@ -617,6 +622,7 @@ __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
         if constexpr (!M::exact_operands) dq[nt] = M::mma(dl, kb_, dq[nt]);
       }
     }
+    if constexpr (D == 128) __builtin_amdgcn_s_setprio(0);
   }
 
   // sum the two key-half partials: kh = 1 hands its accumulators over in LDS
