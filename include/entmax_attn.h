@@ -71,6 +71,7 @@ typedef struct {
  *   q_index    i32   [BH, T, T]    row (b,h,i): Q_i ascending in its first q_count entries
  *   k_count    i32   [BH, T]       |K_j|, query blocks listed for key block j
  *   k_index    i32   [BH, T, T]    row (b,h,j): K_j ascending in its first k_count entries
+ *                                  (k_count, k_index: written only when need_bwd)
  *   stats      i32   [2, BH, T]    optional (may be NULL), per 64-row query block: [0] the K
  *                                  passes the solver streamed (1 max pass + evaluations that
  *                                  did not run on cached scores), [1] its evaluations of
@@ -157,8 +158,8 @@ ea_status entmax_attn_bwd(const ea_shape* shape, const ea_params* params, const 
  *   forward  stage 0: tau, block_mask, q_count/q_index and stats (solver,
  *                     Algorithm 1/3, Eq. 8; row tables, Sec. 3.2.1)
  *            stage 1: O (and o2 if need_bwd) from tau and the row tables
- *                     (Algorithm 2, App. A.5), and k_count/k_index from
- *                     block_mask (Sec. 3.2.1)
+ *                     (Algorithm 2, App. A.5), and if need_bwd
+ *                     k_count/k_index from block_mask (Sec. 3.2.1)
  *   backward stage 0: delta = rowsum(dO * o2) into the workspace (App. A.2)
  *            stage 1: dK, dV over each key block's list (Algorithm 4, Eq. 12-13)
  *            stage 2: dQ over each query block's list (Algorithm 5, Eq. 11)

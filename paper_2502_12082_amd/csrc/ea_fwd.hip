@@ -277,10 +277,13 @@ __global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
   }
 }
 
+// The column tables serve the backward only, so an inference forward
+// (TRAIN false) launches no workgroups for them.
 template <typename E, int D, bool TRAIN>
 hipError_t launch_fwd_dt(const FwdArgs& a, hipStream_t s) {
   const int nqb = a.BH * a.T;
-  dim3 grid((unsigned)(nqb + (nqb + FWD_COLS_PER_WG - 1) / FWD_COLS_PER_WG)), block(FWD_NT);
+  const int ncol = TRAIN ? (nqb + FWD_COLS_PER_WG - 1) / FWD_COLS_PER_WG : 0;
+  dim3 grid((unsigned)(nqb + ncol)), block(FWD_NT);
   auto kernel = fwd_kernel<E, D, 0, TRAIN>;
   if (a.gk == 1) kernel = fwd_kernel<E, D, 1, TRAIN>;
   if (a.gk == 2) kernel = fwd_kernel<E, D, 2, TRAIN>;

@@ -35,7 +35,7 @@ def _full_case(B, H, n, d, dtype, alpha, causal, bwd, c, seed, heads=None, label
     log("case %s B%d H%d n%d d%d %s alpha=%g causal=%d bwd=%d c=%g" % (
         label, B, H, n, d, dtype, alpha, causal, bwd, c))
     gpu = run_gpu(inp, alpha, scale, causal, bwd, heads=heads)
-    check_tables(gpu, causal)
+    check_tables(gpu, causal, columns=bwd)
     errs = []
     for bh in (heads if heads is not None else range(B * H)):
         ref = oracle_head(inp, bh, alpha, scale, causal, bwd)
