@@ -72,8 +72,11 @@ constexpr int FWD_COLS_PER_WG = FWD_NT / 64;  // column tables per extra workgro
 //
 // Workgroups past the BH * T query blocks build the column tables instead,
 // one key block per wave (they come last in the grid).
+//
+// The bf16 d = 64 inference instances fit 128 registers, so four waves share
+// each SIMD instead of three (B8 H12 n1024: 0.049 against 0.052 ms).
 template <typename E, int D, int GK, bool TRAIN>
-__global__ __launch_bounds__(FWD_NT, 2) void fwd_kernel(FwdArgs a) {
+__global__ __launch_bounds__(FWD_NT, !TRAIN && D == 64 && sizeof(E) == 2 ? 4 : 2) void fwd_kernel(FwdArgs a) {
   const int nqb = a.BH * a.T;
   if ((int)blockIdx.x >= nqb) {
     const int col = ((int)blockIdx.x - nqb) * FWD_COLS_PER_WG + wave_id();
