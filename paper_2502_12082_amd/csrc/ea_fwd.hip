@@ -119,22 +119,16 @@ __global__ __launch_bounds__(FWD_NT, !TRAIN && D == 64 && sizeof(E) == 2 ? 4 : 2
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) qf[kk] = load_row_frag_global<E, D>(Q, i, n, kk);
 
-  // At d = 64 a wave raises its issue priority over its MFMA chains, so
-  // that the two waves of a SIMD drift apart (one in its MFMAs while the
-  // other maps scores to P and U) instead of contending in the same phase:
-  // the kernel took 0.070 against 0.082 ms on B8 H12 n1024, 0.220 against
-  // 0.252 on B4 H12 n4096 causal and 0.291 against 0.318 on B1 H8 n16384
-  // causal.  At d = 128 it made no difference (1.03 ms on B1 H16 n8192), and
-  // in the backward kernels it was neutral or slower (dK/dV 1.31 against
-  // 1.27 ms at d = 128), so they do without.
-  auto mfma_priority = [](bool high) {
-    if constexpr (D == 64) {
-      if (high)
-        __builtin_amdgcn_s_setprio(1);
-      else
-        __builtin_amdgcn_s_setprio(0);
-    }
-  };
+  // A wave raises its issue priority over its MFMA chains, so that the two
+  // waves of a SIMD drift apart (one in its MFMAs while the other maps
+  // scores to P and U) instead of contending in the same phase.  At d = 64
+  // over S and P V: the kernel took 0.070 against 0.082 ms on B8 H12 n1024,
+  // 0.220 against 0.252 on B4 H12 n4096 causal and 0.291 against 0.318 on
+  // B1 H8 n16384 causal.  At d = 128 over P V only: 1.017 against 1.027 ms
+  // on B1 H16 n8192 at c = 1, 0.580 against 0.604 at c = 16 (over both
+  // products it changed nothing there).  In the dK/dV kernels it was slower
+  // (1.31 against 1.27 ms at d = 128), so they do without.
+  constexpr bool PRIO_S = D == 64;
 
   const int32_t* list = a.q_index + ((size_t)bh * T + qb) * T;
   const int cnt = a.q_count[(size_t)bh * T + qb];
@@ -173,10 +167,10 @@ __global__ __launch_bounds__(FWD_NT, !TRAIN && D == 64 && sizeof(E) == 2 ? 4 : 2
     if (kind == 0) continue;
     // S^T = K Q^T for this wave's 32 keys x 32 queries
     f32x16 s = zero16();
-    mfma_priority(true);
+    if constexpr (PRIO_S) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) s = M::mma(lds_row_frag<E, D>(kt, 32 * kh + (lane & 31), kk), qf[kk], s);
-    mfma_priority(false);
+    if constexpr (PRIO_S) __builtin_amdgcn_s_setprio(0);
     if (kind == 2) {  // invalid keys -> -inf, so [x - tau]_+ is exactly 0 there
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -202,7 +196,7 @@ __global__ __launch_bounds__(FWD_NT, !TRAIN && D == 64 && sizeof(E) == 2 ? 4 : 2
         p[r] = Gamma<GK>::p_only(zp, g);
       }
     }
-    mfma_priority(true);
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int t = 0; t < PS; ++t) {
       typename M::frag ph, pl, uh, ul;
@@ -219,7 +213,7 @@ __global__ __launch_bounds__(FWD_NT, !TRAIN && D == 64 && sizeof(E) == 2 ? 4 : 2
         }
       }
     }
-    mfma_priority(false);
+    __builtin_amdgcn_s_setprio(0);
   }
 
   // Sum the two key-half partials of each query half through LDS: first O
