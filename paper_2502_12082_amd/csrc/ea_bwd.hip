@@ -502,9 +502,10 @@ constexpr int DQ_NT = 256;
 // partials are summed through LDS at the end.  Halving the per-wave state
 // lets two waves share each SIMD.  At d = 128 a wave raises its issue
 // priority over its dQ products, so that the two waves of a SIMD drift
-// apart (0.905 against 0.922 ms on B1 H16 n8192 at c = 1, 0.505 against
-// 0.531 at c = 16); at d = 64 that was slower (0.256 against 0.252 ms on
-// B1 H8 n16384 causal).
+// apart (B1 H16 n8192: 0.905 against 0.922 ms at alpha = 1.5, c = 1, 0.505
+// against 0.531 at c = 16, 0.925 against 0.941 at alpha = 1.25, c = 1, 0.806
+// against 0.844 at alpha = 2, c = 1); at d = 64 that was slower (0.256
+// against 0.252 ms on B1 H8 n16384 causal).
 template <typename E, int D, int GK>
 __global__ __launch_bounds__(DQ_NT, 2) void dq_kernel(BwdArgs a) {
   using TL = Tile<E, D>;

@@ -126,9 +126,13 @@ __global__ __launch_bounds__(FWD_NT, !TRAIN && D == 64 && sizeof(E) == 2 ? 4 : 2
   // 0.220 against 0.252 on B4 H12 n4096 causal and 0.291 against 0.318 on
   // B1 H8 n16384 causal.  At d = 128 over P V only: 1.017 against 1.027 ms
   // on B1 H16 n8192 at c = 1, 0.580 against 0.604 at c = 16 (over both
-  // products it changed nothing there).  In the dK/dV kernels it was slower
-  // (1.31 against 1.27 ms at d = 128), so they do without.
-  constexpr bool PRIO_S = D == 64;
+  // products it changed nothing there).  Measured for alpha = 1.5 (gamma =
+  // 2) only: at alpha = 1.25 (gamma = 4, more work per score between the
+  // products) the d = 128 kernel got slower (1.38 against 1.29 ms at c = 1)
+  // and at alpha = 2 it made no difference, so the other exponents do
+  // without, as do the dK/dV kernels (1.31 against 1.27 ms at d = 128).
+  constexpr bool PRIO_PV = GK == 2;
+  constexpr bool PRIO_S = PRIO_PV && D == 64;
 
   const int32_t* list = a.q_index + ((size_t)bh * T + qb) * T;
   const int cnt = a.q_count[(size_t)bh * T + qb];
@@ -196,7 +200,7 @@ __global__ __launch_bounds__(FWD_NT, !TRAIN && D == 64 && sizeof(E) == 2 ? 4 : 2
         p[r] = Gamma<GK>::p_only(zp, g);
       }
     }
-    __builtin_amdgcn_s_setprio(1);
+    if constexpr (PRIO_PV) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int t = 0; t < PS; ++t) {
       typename M::frag ph, pl, uh, ul;
@@ -213,7 +217,7 @@ __global__ __launch_bounds__(FWD_NT, !TRAIN && D == 64 && sizeof(E) == 2 ? 4 : 2
         }
       }
     }
-    __builtin_amdgcn_s_setprio(0);
+    if constexpr (PRIO_PV) __builtin_amdgcn_s_setprio(0);
   }
 
   // Sum the two key-half partials of each query half through LDS: first O
