@@ -738,6 +738,7 @@ def main():
         out["other_configs"] = other_configs(args)
     if not args.no_rows:
         out["entmax_rows"] = rows_bench()
+        out["entmax_rows_short"] = rows_bench(rows=65536, n=1024)
         out["no_mask_mode"] = dense_mode_bench(run)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(run, args.cpu_heads)

@@ -8,12 +8,14 @@
 // of p with respect to s is scale * (Diag(u) - u u^T / sum u) (Sec. 3.2.2;
 // (alpha-1) gamma = 1), so ds = scale * u (dp - <u, dp> / sum u).
 //
-// Layout: 256 threads per row; thread t keeps elements 4 (t + 256 w) + e,
-// w < VPT / 4, e < 4, in registers (16-byte accesses when n is a multiple
-// of 8), so the row is read once and every evaluation of the iteration runs
-// from registers, with one workgroup reduction per evaluation.  The forward
-// runs rows of more than 4096 elements in persistent workgroups that load
-// their next row while iterating on the current one.  The update rules are
+// Layout: NT threads per row (a workgroup of 256, or in the forward one
+// wave of 64 for rows of up to 2048 elements); thread t keeps elements
+// 4 (t + NT w) + e, w < VPT / 4, e < 4, in registers (16-byte accesses when
+// n is a multiple of 8), so the row is read once and every evaluation of
+// the iteration runs from registers, with one reduction over the row's
+// threads per evaluation.  The forward runs rows of more than 4096 elements
+// in persistent workgroups that load their next row while iterating on the
+// current one.  The update rules are
 // those of the attention solver: the bracket test with its rounding slack,
 // the Newton lower bound for gamma >= 1 and the midpoint safeguard for
 // gamma < 1.
@@ -93,9 +95,9 @@ __device__ __forceinline__ float wg_max(float v, float* sh) {
 // Element held in slot v of the calling thread: groups of 4 consecutive
 // elements, so that rows whose length is a multiple of 8 move in 16-byte
 // (fp32) or 8-byte (bf16) accesses.
-template <int VPT>
-__device__ __forceinline__ int row_elem(int v) {
-  return 4 * ((int)threadIdx.x + ROW_NT * (v / 4)) + (v % 4);
+template <int VPT, int NT = ROW_NT>
+__device__ __forceinline__ int row_elem(int v, int t = (int)threadIdx.x) {
+  return 4 * (t + NT * (v / 4)) + (v % 4);
 }
 
 // The raw values of a row held for the prefetch: one 16-byte (fp32) or
@@ -130,13 +132,13 @@ struct RawRow {
   }
 };
 
-template <typename E, int VPT>
-__device__ __forceinline__ void load_row(const E* s, int n, float c, float (&x)[VPT]) {
+template <typename E, int VPT, int NT = ROW_NT>
+__device__ __forceinline__ void load_row(const E* s, int n, float c, float (&x)[VPT], int t = (int)threadIdx.x) {
   static_assert(VPT % 4 == 0, "slots come in groups of 4");
   const bool vec = (n % 8) == 0;
 #pragma unroll
   for (int g4 = 0; g4 < VPT / 4; ++g4) {
-    const int j0 = row_elem<VPT>(4 * g4);
+    const int j0 = row_elem<VPT, NT>(4 * g4, t);
     if (vec && j0 < n) {
       if constexpr (sizeof(E) == 4) {
         const f32x4 v4 = *reinterpret_cast<const f32x4*>(s + j0);
@@ -156,12 +158,12 @@ __device__ __forceinline__ void load_row(const E* s, int n, float c, float (&x)[
 }
 
 // Stores slot values y to row r (length n) in the same element order.
-template <int VPT>
-__device__ __forceinline__ void store_row(float* r, int n, const float (&y)[VPT]) {
+template <int VPT, int NT = ROW_NT>
+__device__ __forceinline__ void store_row(float* r, int n, const float (&y)[VPT], int t = (int)threadIdx.x) {
   const bool vec = (n % 8) == 0;
 #pragma unroll
   for (int g4 = 0; g4 < VPT / 4; ++g4) {
-    const int j0 = row_elem<VPT>(4 * g4);
+    const int j0 = row_elem<VPT, NT>(4 * g4, t);
     if (vec && j0 < n) {
       *reinterpret_cast<f32x4*>(r + j0) = f32x4{y[4 * g4], y[4 * g4 + 1], y[4 * g4 + 2], y[4 * g4 + 3]};
     } else {
@@ -170,6 +172,109 @@ __device__ __forceinline__ void store_row(float* r, int n, const float (&y)[VPT]
         if (j0 + e < n) r[j0 + e] = y[4 * g4 + e];
     }
   }
+}
+
+// Reductions over the threads that hold one row: a workgroup through LDS
+// (LDS_ONLY: with a barrier that leaves global loads in flight), or a single
+// wave through lane exchanges alone.  Every thread receives the totals; the
+// exchanges add commutative pairs, so all lanes hold the same bits.
+template <bool LDS_ONLY>
+struct WgRed {
+  float* sh;
+  __device__ __forceinline__ float max(float v) const { return wg_max<LDS_ONLY>(v, sh); }
+  __device__ __forceinline__ Sums sum(Sums v) const { return wg_sum<LDS_ONLY>(v, sh); }
+};
+
+struct WaveRed {
+  __device__ __forceinline__ float max(float v) const {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+  }
+  __device__ __forceinline__ Sums sum(Sums v) const {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      v.a += __shfl_xor(v.a, o);
+      v.b += __shfl_xor(v.b, o);
+      v.c += __shfl_xor(v.c, o);
+      v.k += __shfl_xor(v.k, o);
+    }
+    return v;
+  }
+};
+
+// Algorithm 1 on one row: tau for the scaled scores x this thread holds
+// (-inf past the end of the row), the row's other values held by the
+// threads that `red` reduces over.
+template <int VPT, int GK, typename Red>
+__device__ __forceinline__ float row_tau(const float (&x)[VPT], int n, const RowsArgs& a, const Red& red) {
+  const float g = a.gamma;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < VPT; ++v) mx = fmaxf(mx, x[v]);
+  const float m = red.max(mx);
+
+  // Algorithm 1: bracket [m - 1, m - n^(1-alpha)], first tau at its midpoint
+  float lo = m - 1.f, hi = m - powf((float)n, 1.f - a.alpha);
+  float tau = 0.5f * (lo + hi);
+  const bool newton_bound = g >= 1.f;
+  float f_prev = INFINITY;
+  for (int it = 0;; ++it) {
+    Sums t{0.f, 0.f, 0.f, 0};
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) {
+      const float zp = __builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f);
+      if constexpr (GK == 1) {
+        t.a += zp;
+        t.k += in_support(zp);
+      } else if constexpr (GK == 2) {
+        t.a = fmaf(zp, zp, t.a);
+        t.b += zp;
+        t.k += in_support(zp);
+      } else if constexpr (GK == 4) {
+        const float z2 = zp * zp;
+        t.a = fmaf(z2, z2, t.a);
+        t.b = fmaf(z2, zp, t.b);
+        t.c += z2;
+      } else {
+        if (zp > 0.f) {
+          const float l = __log2f(zp);
+          t.a += exp2f(g * l);
+          t.b += exp2f((g - 1.f) * l);
+          t.c += exp2f((g - 2.f) * l);
+        }
+      }
+    }
+    const Sums tot = red.sum(t);
+    const float f = tot.a - 1.f;  // Eq. 3
+    float f1, f2;                 // Eq. 6, 7
+    if constexpr (GK == 1) {
+      f1 = -(float)tot.k;
+      f2 = 0.f;
+    } else if constexpr (GK == 2) {
+      f1 = -2.f * tot.b;
+      f2 = 2.f * (float)tot.k;
+    } else if constexpr (GK == 4) {
+      f1 = -4.f * tot.b;
+      f2 = 12.f * tot.c;
+    } else {
+      f1 = -g * tot.b;
+      f2 = g * (g - 1.f) * tot.c;
+    }
+    if (fabsf(f) <= a.tol || it >= a.max_iter) break;
+    if (f < 0.f)  // B_f, Eq. 4
+      hi = tau;
+    else
+      lo = tau;
+    const float slack = 1e-6f * fmaxf(1.f, fmaxf(fabsf(lo), fabsf(hi)));
+    if (newton_bound && f1 < 0.f) lo = fminf(fmaxf(lo, tau - f / f1 - 10.f * slack), hi);
+    const float th = tau - 2.f * f * f1 / (2.f * f1 * f1 - f * f2);  // H_f, Eq. 5
+    bool take = th >= lo - slack && th <= hi + slack;
+    if (!newton_bound && fabsf(f) > 0.5f * f_prev) take = false;
+    f_prev = fabsf(f);
+    tau = take ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
+  }
+  return tau;
 }
 
 // PF (rows of more than 4096 elements, a multiple of 8): persistent
@@ -190,72 +295,7 @@ __global__ __launch_bounds__(ROW_NT) void rows_fwd_kernel(RowsArgs a) {
   const E* S = static_cast<const E*>(a.s);
   // Algorithm 1 on row `row`, whose scaled scores are x; writes p and tau.
   auto solve_row = [&](size_t row, float (&x)[VPT]) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int v = 0; v < VPT; ++v) mx = fmaxf(mx, x[v]);
-    const float m = wg_max<PF>(mx, sh);
-
-    // Algorithm 1: bracket [m - 1, m - n^(1-alpha)], first tau at its midpoint
-    float lo = m - 1.f, hi = m - powf((float)n, 1.f - a.alpha);
-    float tau = 0.5f * (lo + hi);
-    const bool newton_bound = g >= 1.f;
-    float f_prev = INFINITY;
-    for (int it = 0;; ++it) {
-      Sums t{0.f, 0.f, 0.f, 0};
-#pragma unroll
-      for (int v = 0; v < VPT; ++v) {
-        const float zp = __builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f);
-        if constexpr (GK == 1) {
-          t.a += zp;
-          t.k += in_support(zp);
-        } else if constexpr (GK == 2) {
-          t.a = fmaf(zp, zp, t.a);
-          t.b += zp;
-          t.k += in_support(zp);
-        } else if constexpr (GK == 4) {
-          const float z2 = zp * zp;
-          t.a = fmaf(z2, z2, t.a);
-          t.b = fmaf(z2, zp, t.b);
-          t.c += z2;
-        } else {
-          if (zp > 0.f) {
-            const float l = __log2f(zp);
-            t.a += exp2f(g * l);
-            t.b += exp2f((g - 1.f) * l);
-            t.c += exp2f((g - 2.f) * l);
-          }
-        }
-      }
-      const Sums tot = wg_sum<PF>(t, sh);
-      const float f = tot.a - 1.f;  // Eq. 3
-      float f1, f2;                 // Eq. 6, 7
-      if constexpr (GK == 1) {
-        f1 = -(float)tot.k;
-        f2 = 0.f;
-      } else if constexpr (GK == 2) {
-        f1 = -2.f * tot.b;
-        f2 = 2.f * (float)tot.k;
-      } else if constexpr (GK == 4) {
-        f1 = -4.f * tot.b;
-        f2 = 12.f * tot.c;
-      } else {
-        f1 = -g * tot.b;
-        f2 = g * (g - 1.f) * tot.c;
-      }
-      if (fabsf(f) <= a.tol || it >= a.max_iter) break;
-      if (f < 0.f)  // B_f, Eq. 4
-        hi = tau;
-      else
-        lo = tau;
-      const float slack = 1e-6f * fmaxf(1.f, fmaxf(fabsf(lo), fabsf(hi)));
-      if (newton_bound && f1 < 0.f) lo = fminf(fmaxf(lo, tau - f / f1 - 10.f * slack), hi);
-      const float th = tau - 2.f * f * f1 / (2.f * f1 * f1 - f * f2);  // H_f, Eq. 5
-      bool take = th >= lo - slack && th <= hi + slack;
-      if (!newton_bound && fabsf(f) > 0.5f * f_prev) take = false;
-      f_prev = fabsf(f);
-      tau = take ? fminf(fmaxf(th, lo), hi) : 0.5f * (lo + hi);
-    }
-
+    const float tau = row_tau<VPT, GK>(x, n, a, WgRed<PF>{sh});
     float pv[VPT];
 #pragma unroll
     for (int v = 0; v < VPT; ++v) pv[v] = Gamma<GK>::p_only(__builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f), g);
@@ -278,6 +318,26 @@ __global__ __launch_bounds__(ROW_NT) void rows_fwd_kernel(RowsArgs a) {
     load_row<E, VPT>(S + (size_t)blockIdx.x * n, n, c, x);
     solve_row(blockIdx.x, x);
   }
+}
+
+// Rows of up to 2048 elements: one wave per row, four rows per workgroup,
+// reductions by lane exchanges alone (no barriers), so that a workgroup's
+// rows do not wait for each other (65536 x 1024 fp32: 0.102 against 0.230
+// ms with a workgroup per row; tau differs from that kernel's in the last
+// bits, its sums being added in another order).
+template <typename E, int VPT, int GK>
+__global__ __launch_bounds__(ROW_NT) void rows_fwd_wave_kernel(RowsArgs a) {
+  const int64_t row = (int64_t)blockIdx.x * (ROW_NT / 64) + wave_id();
+  if (row >= a.rows) return;  // whole waves: the kernel has no barrier
+  const int n = a.n, t = lane_id();
+  float x[VPT];
+  load_row<E, VPT, 64>(static_cast<const E*>(a.s) + (size_t)row * n, n, a.c, x, t);
+  const float tau = row_tau<VPT, GK>(x, n, a, WaveRed{});
+  float pv[VPT];
+#pragma unroll
+  for (int v = 0; v < VPT; ++v) pv[v] = Gamma<GK>::p_only(__builtin_amdgcn_fmed3f(x[v] - tau, 0.f, 1.f), a.gamma);
+  store_row<VPT, 64>(a.p + (size_t)row * n, n, pv, t);
+  if (t == 0) a.tau[row] = tau;
 }
 
 template <typename E, int VPT, int GK>
@@ -343,9 +403,25 @@ hipError_t launch_rows_v(const RowsArgs& a, hipStream_t s) {
   }
 }
 
-// The smallest register row that holds n elements.
+template <typename E, int VPT>
+hipError_t launch_rows_wave(const RowsArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)((a.rows + ROW_NT / 64 - 1) / (ROW_NT / 64))), block(ROW_NT);
+  auto kernel = rows_fwd_wave_kernel<E, VPT, 0>;
+  if (a.gk == 1) kernel = rows_fwd_wave_kernel<E, VPT, 1>;
+  if (a.gk == 2) kernel = rows_fwd_wave_kernel<E, VPT, 2>;
+  if (a.gk == 4) kernel = rows_fwd_wave_kernel<E, VPT, 4>;
+  return launch_kernel(kernel, grid, block, s, a);
+}
+
+// The smallest register row that holds n elements: a wave's for forward
+// rows of up to 2048 elements, else a workgroup's.
 template <typename E, bool BWD>
 hipError_t launch_rows_e(const RowsArgs& a, hipStream_t s) {
+  if (!BWD) {
+    if (a.n <= 64 * 4) return launch_rows_wave<E, 4>(a, s);
+    if (a.n <= 64 * 16) return launch_rows_wave<E, 16>(a, s);
+    if (a.n <= 64 * 32) return launch_rows_wave<E, 32>(a, s);
+  }
   if (a.n <= ROW_NT * 4) return launch_rows_v<E, 4, BWD>(a, s);
   if (a.n <= ROW_NT * 16) return launch_rows_v<E, 16, BWD>(a, s);
   if (a.n <= ROW_NT * 32) return launch_rows_v<E, 32, BWD>(a, s);

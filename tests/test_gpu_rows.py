@@ -59,7 +59,7 @@ def _case(rows, n, dtype, alpha, sigma, seed, scale=1.0, bwd=True):
         assert worst["ds"] <= GRAD_REL
 
 
-@pytest.mark.parametrize("n", [1, 2, 255, 256, 257, 1000, 1024, 4096, 8192, 16384, 32768])
+@pytest.mark.parametrize("n", [1, 2, 255, 256, 257, 1000, 1024, 2048, 2049, 4096, 8192, 16384, 32768])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_rows_shapes(n, dtype):
     _case(5, n, dtype, 1.5, 1.0, synth.SEED_BASE + 10)
