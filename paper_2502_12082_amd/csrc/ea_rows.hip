@@ -282,11 +282,11 @@ __device__ __forceinline__ float row_tau(const float (&x)[VPT], int n, const Row
 // values are loaded into registers while the current row iterates, so that
 // a workgroup's loads overlap its own iterations (8192 x 8192: 0.108
 // against 0.111 ms in fp32, 0.082 against 0.087 ms in bf16; 4096 x 32768
-// fp32: 0.235 against 0.269 ms).  Otherwise one
-// workgroup per row: for shorter rows the prefetch registers cost occupancy
-// and the persistent loop was slower (65536 x 1024: 0.253 against 0.229 ms).
-// (The backward, one reduction per row, got slower the same way: 0.175
-// against 0.139 ms at 8192 x 8192.)
+// fp32: 0.235 against 0.269 ms).  Otherwise one workgroup per row: for
+// shorter rows the prefetch registers cost occupancy and the persistent
+// loop was slower (65536 x 1024: 0.253 against 0.229 ms).  (The backward,
+// one reduction per row, got slower the same way: 0.175 against 0.139 ms at
+// 8192 x 8192.)
 template <typename E, int VPT, int GK, bool PF>
 __global__ __launch_bounds__(ROW_NT) void rows_fwd_kernel(RowsArgs a) {
   __shared__ float sh[4 * (ROW_NT / 64)];
